@@ -1,0 +1,164 @@
+/*
+ * disdp.h -- C ABI of the parameter-server hot path of DisDP
+ * (arXiv 2409.00918) on one MI355X (gfx950).
+ *
+ * In DisDP each worker pushes its partial gradient of a model layer, the
+ * SmartSwitch sums the W contributions in the network, and a parameter
+ * server pulls the aggregate, runs a mixed-precision Adam step on its
+ * 12-byte model states and serves the 2-byte parameter copy back
+ * (Section III-A "Overall Architecture"; Section III-D "Backward Stage",
+ * steps 3, 5 and 1-2; Table III).  This library performs that reduction and
+ * that optimizer step on one GPU, for one shard of N elements whose W
+ * contributions already sit in device memory:
+ *
+ *   disdp_aggregate      -- the W-way reduction alone (the switch's job),
+ *   disdp_adam_step      -- the optimizer step alone (step 5),
+ *   disdp_aggregate_adam -- both in one pass over memory, with the bf16
+ *                           parameter copy fused into the store.
+ *
+ * The calls follow the shape of the paper's asynchronous push/pull API
+ * (Table II: a buffer pointer and a length; completion awaited through a
+ * handle): a HIP stream plays the role of the handle.
+ *
+ * Common conventions
+ * ------------------
+ * Ownership   The caller owns every buffer.  The library allocates nothing,
+ *             keeps no state between calls, never synchronises and is
+ *             re-entrant.  Array pointers are DEVICE pointers (memory the
+ *             GPU can read and write); `grads` itself is a HOST array of W
+ *             device pointers and is read before the call returns.
+ * Layout      Every array is flat and contiguous with N elements; index i
+ *             is the same parameter in every array.  fp32 arrays hold IEEE
+ *             binary32; bf16 arrays hold raw bf16 bit patterns (uint16_t);
+ *             the int32 aggregate is two's complement.
+ * Asynchrony  Work is enqueued on `stream` (0 = the null stream) and the
+ *             call returns at once; completion is the caller's
+ *             hipStreamSynchronize or an event.
+ * Alignment   Any alignment is accepted.  When every pointer is 16-byte
+ *             aligned (8-byte for bf16 arrays) the vector kernels run,
+ *             otherwise element-wise ones; results are identical.
+ * Errors      Arguments are checked on the host before any HIP call, in
+ *             this order: counts and enumerations, hyperparameters, then
+ *             (only when n > 0) NULL pointers, then overlap.  A failed check
+ *             returns its code and enqueues nothing.  n == 0 returns
+ *             DISDP_OK with no launch (NULL pointers are then allowed).
+ *             Outputs must not overlap one another nor any input; p, m and
+ *             v are updated in place (each is its own input).  Contributions
+ *             may overlap each other (the same buffer may be passed twice).
+ *             A launch failure returns DISDP_ERR_HIP.
+ * Numerics    IEEE binary32, round to nearest even, one rounding per
+ *             operation, no fused multiply-add, denormals kept; results are
+ *             a deterministic function of the inputs (no atomics, no
+ *             dependence on grid size).
+ */
+#ifndef DISDP_H
+#define DISDP_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    DISDP_OK = 0,
+    DISDP_ERR_INVALID_ARG = 1, /* bad count, range, hyperparameter or NULL */
+    DISDP_ERR_UNSUPPORTED = 2, /* unknown dtype or aggregation mode        */
+    DISDP_ERR_ALIAS = 3,       /* an output overlaps another buffer        */
+    DISDP_ERR_HIP = 4          /* the HIP runtime refused the launch       */
+} disdp_status_t;
+
+/* Element type of the W gradient contributions.  Workers produce fp16/bf16
+ * or fp32 gradients (Section III-B "Format Conversion Unit"); bf16 is
+ * widened to fp32 exactly before any arithmetic. */
+typedef enum { DISDP_DT_F32 = 0, DISDP_DT_BF16 = 1 } disdp_dtype_t;
+
+/* How the W contributions are summed.
+ *  DISDP_AGG_FP32   acc = g_0[i]; acc = acc + g_w[i] for w = 1 .. W-1, in
+ *                   fp32, always in this worker order.
+ *  DISDP_AGG_FIXED  the integer format an integer-only switch sums
+ *                   (Section III-B, following SwitchML): each contribution
+ *                   becomes q_w = sat32(round_half_even(g_w[i] * 2^k))
+ *                   (NaN -> 0, +-inf and out-of-range values saturate);
+ *                   S = sum of q_w in 64-bit integers (exact, so independent
+ *                   of the order contributions arrive in); A = sat32(S);
+ *                   the float aggregate is (float)A * 2^-k. */
+typedef enum { DISDP_AGG_FP32 = 0, DISDP_AGG_FIXED = 1 } disdp_agg_mode_t;
+
+/* Adam with decoupled weight decay (Section III-D, step 5: 17 flops per
+ * element on the aggregated gradient and the fp32 master weight, m and v).
+ * With g = agg * grad_scale and t = step:
+ *   m = beta1 m + (1 - beta1) g
+ *   v = beta2 v + (1 - beta2) g^2
+ *   p = p (1 - lr weight_decay) - lr (m / (1 - beta1^t)) / (sqrt(v / (1 - beta2^t)) + eps)
+ * 1 - beta^t and 1 - lr weight_decay are evaluated in double on the host
+ * and rounded once to fp32; 1 - beta is an fp32 subtraction.
+ * Valid ranges: step >= 1; 0 <= beta1, beta2 < 1; eps >= 0; all values
+ * finite.  eps == 0 is accepted: then a zero gradient with v == 0 gives
+ * 0/0 = NaN, as IEEE arithmetic does. */
+typedef struct {
+    float lr;
+    float beta1;
+    float beta2;
+    float eps;
+    float weight_decay;
+    int64_t step;      /* t >= 1; the caller counts steps */
+    float grad_scale;  /* applied to the aggregate; 1.0f = plain sum */
+} disdp_adamw_hparams_t;
+
+/* W-way reduction of one shard (the SmartSwitch's aggregation, Section
+ * III-A and III-C "Packet Transport Procedure").
+ *   grads       host array of W device pointers, each to n elements of
+ *               `gdtype`; 1 <= W <= 64.
+ *   mode        DISDP_AGG_FP32 or DISDP_AGG_FIXED; frac_bits = k in [0, 30]
+ *               (checked in fixed mode only).
+ *   agg_out_f32 fp32 aggregate (n elements).  Required in FP32 mode.
+ *   agg_out_i32 int32 aggregate A (n elements); fixed mode only, must be
+ *               NULL in FP32 mode.  In fixed mode at least one of the two
+ *               outputs must be non-NULL.
+ * Returns DISDP_OK or an error code (see the conventions above). */
+disdp_status_t disdp_aggregate(const void *const *grads, int W,
+                               disdp_dtype_t gdtype, int64_t n,
+                               disdp_agg_mode_t mode, int frac_bits,
+                               float *agg_out_f32, int32_t *agg_out_i32,
+                               hipStream_t stream);
+
+/* The optimizer step alone on an already aggregated fp32 gradient
+ * (Section III-D, step 5: reads a gradient and 12 bytes of state, writes
+ * 12 bytes of state and a 2-byte parameter copy).
+ *   grad            fp32 aggregate (n elements), read only.
+ *   param, m, v     fp32 master weight and moments, updated in place.
+ *   param_bf16_out  bf16 copy of the updated weight, round to nearest even
+ *                   (NaN keeps its sign, becomes 0x7FC0 | sign); NULL = skip.
+ *   hp              host pointer, read before the call returns. */
+disdp_status_t disdp_adam_step(const float *grad, float *param, float *m,
+                               float *v, uint16_t *param_bf16_out, int64_t n,
+                               const disdp_adamw_hparams_t *hp,
+                               hipStream_t stream);
+
+/* Aggregation and optimizer step fused into one pass: each element's W
+ * contributions, p, m and v are read once and p, m, v and the bf16 copy
+ * written once.  Equal, bit for bit, to disdp_aggregate followed by
+ * disdp_adam_step on its fp32 aggregate.
+ *   agg_out_f32 / agg_out_i32   optional copies of the aggregate (NULL = not
+ *               written; agg_out_i32 only in fixed mode).
+ * Other arguments as in disdp_aggregate and disdp_adam_step. */
+disdp_status_t disdp_aggregate_adam(const void *const *grads, int W,
+                                    disdp_dtype_t gdtype, int64_t n,
+                                    disdp_agg_mode_t mode, int frac_bits,
+                                    float *param, float *m, float *v,
+                                    uint16_t *param_bf16_out,
+                                    float *agg_out_f32, int32_t *agg_out_i32,
+                                    const disdp_adamw_hparams_t *hp,
+                                    hipStream_t stream);
+
+/* A static, NUL-terminated English name for a status code (never NULL;
+ * unknown codes give "unknown status"). */
+const char *disdp_status_string(disdp_status_t status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DISDP_H */

@@ -1,0 +1,262 @@
+"""Python binding of libdisdp: the DisDP parameter-server hot path on MI355X.
+
+Thin ctypes marshalling over the C ABI declared in ``include/disdp.h``: the
+functions below turn torch device tensors into pointers, lengths and the
+current HIP stream and call the library.  Every step of the path -- the W-way
+reduction of the gradient contributions (the SmartSwitch's aggregation,
+Sections III-A and III-C of arXiv 2409.00918, in fp32 or in the integer format
+of Section III-B), the Adam step with decoupled weight decay and the bf16
+parameter copy (Section III-D, step 5) -- runs in the library's HIP kernels.
+There is no other implementation here: if ``libdisdp.so`` is missing, every
+call raises.
+
+``aggregate``       -- the reduction alone            (disdp_aggregate)
+``adam_step``       -- the optimizer step alone       (disdp_adam_step)
+``aggregate_adam``  -- both in one pass               (disdp_aggregate_adam)
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libdisdp.so")
+
+# Status codes, dtypes and modes (values fixed by include/disdp.h).
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_ALIAS, ERR_HIP = 0, 1, 2, 3, 4
+DT_F32, DT_BF16 = 0, 1
+AGG_FP32, AGG_FIXED = 0, 1
+MAX_W = 64
+
+EXPORTS = ("disdp_aggregate", "disdp_adam_step", "disdp_aggregate_adam",
+           "disdp_status_string")
+
+
+class AdamWHParams(ctypes.Structure):
+    """disdp_adamw_hparams_t."""
+    _fields_ = [("lr", ctypes.c_float), ("beta1", ctypes.c_float),
+                ("beta2", ctypes.c_float), ("eps", ctypes.c_float),
+                ("weight_decay", ctypes.c_float), ("step", ctypes.c_int64),
+                ("grad_scale", ctypes.c_float)]
+
+
+class DisdpError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(f"{what}: {status_string(status)} (status {status})")
+
+
+_lib = None
+
+
+def hip_runtimes_mapped() -> list:
+    """Paths of every HIP runtime library mapped into this process."""
+    with open("/proc/self/maps") as f:
+        return sorted({line.split()[-1] for line in f
+                       if "libamdhip64" in line.rsplit("/", 1)[-1]})
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libdisdp.so.  Raises if it has not been built.
+
+    torch ships its own HIP runtime under the same soname as the system one
+    (libamdhip64.so.7).  torch is imported first so that the library's
+    dependency binds to that already-loaded runtime: loaded the other way
+    round, the process would hold two HIP runtimes and the library's launches
+    would go to one that does not own torch's memory and streams."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                f"{LIB_PATH} is missing: build it with "
+                "`python -m paper_2409_00918_amd.build` (hipcc, gfx950)")
+        import torch  # noqa: F401  (binds libamdhip64.so.7 to torch's runtime)
+        L = ctypes.CDLL(LIB_PATH)
+        runtimes = hip_runtimes_mapped()
+        if len(runtimes) > 1:
+            raise RuntimeError(
+                "two HIP runtimes are loaded in this process "
+                f"({', '.join(runtimes)}); load libdisdp through this module "
+                "after importing torch, not before")
+        vp, i64, ci = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
+        L.disdp_aggregate.restype = ci
+        L.disdp_aggregate.argtypes = [vp, ci, ci, i64, ci, ci, vp, vp, vp]
+        L.disdp_adam_step.restype = ci
+        L.disdp_adam_step.argtypes = [vp, vp, vp, vp, vp, i64,
+                                      ctypes.POINTER(AdamWHParams), vp]
+        L.disdp_aggregate_adam.restype = ci
+        L.disdp_aggregate_adam.argtypes = [vp, ci, ci, i64, ci, ci, vp, vp, vp,
+                                           vp, vp, vp,
+                                           ctypes.POINTER(AdamWHParams), vp]
+        L.disdp_status_string.restype = ctypes.c_char_p
+        L.disdp_status_string.argtypes = [ci]
+        _lib = L
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().disdp_status_string(int(status)).decode()
+
+
+# ------------------------------------------------------------ raw calls --
+# Integer pointers and sizes exactly as the C ABI takes them; used by the
+# tensor wrappers below and by the ABI tests.
+def _ptr_array(ptrs: Sequence[int]):
+    return (ctypes.c_void_p * max(1, len(ptrs)))(*[p or None for p in ptrs])
+
+
+def raw_aggregate(grad_ptrs, W, gdtype, n, mode, frac_bits, agg_f32, agg_i32,
+                  stream) -> int:
+    arr = None if grad_ptrs is None else _ptr_array(grad_ptrs)
+    return lib().disdp_aggregate(arr, W, gdtype, n, mode, frac_bits,
+                                 agg_f32 or None, agg_i32 or None,
+                                 stream or None)
+
+
+def raw_adam_step(grad, param, m, v, p16, n, hp: Optional[AdamWHParams],
+                  stream) -> int:
+    return lib().disdp_adam_step(grad or None, param or None, m or None,
+                                 v or None, p16 or None, n,
+                                 None if hp is None else ctypes.byref(hp),
+                                 stream or None)
+
+
+def raw_aggregate_adam(grad_ptrs, W, gdtype, n, mode, frac_bits, param, m, v,
+                       p16, agg_f32, agg_i32, hp: Optional[AdamWHParams],
+                       stream) -> int:
+    arr = None if grad_ptrs is None else _ptr_array(grad_ptrs)
+    return lib().disdp_aggregate_adam(
+        arr, W, gdtype, n, mode, frac_bits, param or None, m or None,
+        v or None, p16 or None, agg_f32 or None, agg_i32 or None,
+        None if hp is None else ctypes.byref(hp), stream or None)
+
+
+# --------------------------------------------------------- torch tensors --
+def _torch():
+    import torch
+    return torch
+
+
+def _mode(mode) -> int:
+    if mode in (AGG_FP32, "fp32"):
+        return AGG_FP32
+    if mode in (AGG_FIXED, "fixed"):
+        return AGG_FIXED
+    raise ValueError(f"unknown aggregation mode {mode!r}")
+
+
+def _grad_dtype(t) -> int:
+    torch = _torch()
+    if t.dtype == torch.float32:
+        return DT_F32
+    if t.dtype in (torch.bfloat16, torch.int16, torch.uint16):
+        return DT_BF16
+    raise TypeError(f"unsupported gradient dtype {t.dtype}")
+
+
+def _dev_ptr(t, name: str, n: int, dtypes) -> int:
+    if t is None:
+        return 0
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.numel() != n:
+        raise ValueError(f"{name} has {t.numel()} elements, expected {n}")
+    if t.dtype not in dtypes:
+        raise TypeError(f"{name} has dtype {t.dtype}")
+    return t.data_ptr()
+
+
+def _stream(stream, ref) -> int:
+    torch = _torch()
+    if stream is None:
+        return torch.cuda.current_stream(ref.device).cuda_stream
+    return getattr(stream, "cuda_stream", stream)
+
+
+def _hparams(lr, beta1, beta2, eps, weight_decay, step, grad_scale):
+    return AdamWHParams(lr, beta1, beta2, eps, weight_decay, int(step),
+                        grad_scale)
+
+
+def _check(status: int, what: str) -> None:
+    if status != OK:
+        raise DisdpError(status, what)
+
+
+def _grads(grads):
+    torch = _torch()
+    grads = list(grads)
+    if not grads:
+        raise ValueError("at least one contribution is needed")
+    n = grads[0].numel()
+    gdt = _grad_dtype(grads[0])
+    allowed = (torch.float32,) if gdt == DT_F32 else \
+        (torch.bfloat16, torch.int16, torch.uint16)
+    ptrs = [_dev_ptr(g, f"grads[{i}]", n, allowed) for i, g in enumerate(grads)]
+    return grads, ptrs, gdt, n
+
+
+def aggregate(grads, *, mode="fp32", frac_bits: int = 0, agg_out_f32=None,
+              agg_out_i32=None, stream=None) -> None:
+    """W-way reduction of `grads` (float32 or bf16 device tensors of one
+    length) into `agg_out_f32` and/or `agg_out_i32` (int32, fixed mode)."""
+    torch = _torch()
+    grads, ptrs, gdt, n = _grads(grads)
+    st = raw_aggregate(ptrs, len(grads), gdt, n, _mode(mode), frac_bits,
+                       _dev_ptr(agg_out_f32, "agg_out_f32", n, (torch.float32,)),
+                       _dev_ptr(agg_out_i32, "agg_out_i32", n, (torch.int32,)),
+                       _stream(stream, grads[0]))
+    _check(st, "disdp_aggregate")
+
+
+def adam_step(grad, param, m, v, param_bf16_out=None, *, lr, beta1, beta2,
+              eps, weight_decay, step, grad_scale=1.0, stream=None) -> None:
+    """One AdamW step on (param, m, v) in place from the fp32 aggregate."""
+    torch = _torch()
+    n = param.numel()
+    f32 = (torch.float32,)
+    st = raw_adam_step(
+        _dev_ptr(grad, "grad", n, f32), _dev_ptr(param, "param", n, f32),
+        _dev_ptr(m, "m", n, f32), _dev_ptr(v, "v", n, f32),
+        _dev_ptr(param_bf16_out, "param_bf16_out", n,
+                 (torch.bfloat16, torch.int16, torch.uint16)),
+        n, _hparams(lr, beta1, beta2, eps, weight_decay, step, grad_scale),
+        _stream(stream, param))
+    _check(st, "disdp_adam_step")
+
+
+def aggregate_adam(grads, param, m, v, param_bf16_out=None, *, lr, beta1,
+                   beta2, eps, weight_decay, step, grad_scale=1.0,
+                   mode="fp32", frac_bits: int = 0, agg_out_f32=None,
+                   agg_out_i32=None, stream=None) -> None:
+    """Aggregate `grads` and take one AdamW step, in one pass."""
+    torch = _torch()
+    grads, ptrs, gdt, n = _grads(grads)
+    f32 = (torch.float32,)
+    st = raw_aggregate_adam(
+        ptrs, len(grads), gdt, n, _mode(mode), frac_bits,
+        _dev_ptr(param, "param", n, f32), _dev_ptr(m, "m", n, f32),
+        _dev_ptr(v, "v", n, f32),
+        _dev_ptr(param_bf16_out, "param_bf16_out", n,
+                 (torch.bfloat16, torch.int16, torch.uint16)),
+        _dev_ptr(agg_out_f32, "agg_out_f32", n, f32),
+        _dev_ptr(agg_out_i32, "agg_out_i32", n, (torch.int32,)),
+        _hparams(lr, beta1, beta2, eps, weight_decay, step, grad_scale),
+        _stream(stream, grads[0]))
+    _check(st, "disdp_aggregate_adam")
+
+
+def algorithmic_bytes_per_element(W: int, grad_bytes: int, adam: bool = True,
+                                  bf16_copy: bool = True, agg_f32: bool = False,
+                                  agg_i32: bool = False) -> int:
+    """Bytes one element moves through HBM in one call, each byte counted
+    once: W contributions read; with the optimizer, p, m, v read and written
+    (12 + 12) and the bf16 copy written (2); optional aggregates written."""
+    b = W * grad_bytes
+    if adam:
+        b += 24 + (2 if bf16_copy else 0)
+    b += (4 if agg_f32 else 0) + (4 if agg_i32 else 0)
+    return b

@@ -1,0 +1,226 @@
+// C-ABI front end of libdisdp: argument checks (host only, before any HIP
+// call), the per-step optimizer constants, and the choice between the
+// vector and element-wise kernels.  The ABI itself is documented in
+// include/disdp.h.
+#include "disdp.h"
+
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+
+#include "disdp_launch.h"
+
+namespace {
+
+using disdp::LaunchArgs;
+
+struct Span {
+    uintptr_t lo, hi;  // [lo, hi)
+};
+
+Span span_of(const void *p, int64_t n, int elem_bytes)
+{
+    uintptr_t lo = reinterpret_cast<uintptr_t>(p);
+    return Span{lo, lo + static_cast<uintptr_t>(n) * static_cast<uintptr_t>(elem_bytes)};
+}
+
+bool overlaps(Span a, Span b) { return a.lo < b.hi && b.lo < a.hi; }
+
+int grad_bytes(int gdtype) { return gdtype == DISDP_DT_BF16 ? 2 : 4; }
+
+// Largest n accepted: keeps every byte count far below 2^63.
+constexpr int64_t kMaxN = int64_t(1) << 56;
+
+disdp_status_t check_counts(int W, int gdtype, int64_t n, int mode, int frac_bits)
+{
+    if (n < 0 || n > kMaxN || W < 1 || W > disdp::kMaxW)
+        return DISDP_ERR_INVALID_ARG;
+    if (gdtype != DISDP_DT_F32 && gdtype != DISDP_DT_BF16)
+        return DISDP_ERR_UNSUPPORTED;
+    if (mode != DISDP_AGG_FP32 && mode != DISDP_AGG_FIXED)
+        return DISDP_ERR_UNSUPPORTED;
+    if (mode == DISDP_AGG_FIXED && (frac_bits < 0 || frac_bits > 30))
+        return DISDP_ERR_INVALID_ARG;
+    return DISDP_OK;
+}
+
+disdp_status_t check_hparams(const disdp_adamw_hparams_t *hp)
+{
+    if (!hp)
+        return DISDP_ERR_INVALID_ARG;
+    if (hp->step < 1)
+        return DISDP_ERR_INVALID_ARG;
+    // written so that NaN fails every test
+    if (!(hp->beta1 >= 0.0f && hp->beta1 < 1.0f) ||
+        !(hp->beta2 >= 0.0f && hp->beta2 < 1.0f))
+        return DISDP_ERR_INVALID_ARG;
+    if (!(hp->eps >= 0.0f) || !std::isfinite(hp->eps) || !std::isfinite(hp->lr) ||
+        !std::isfinite(hp->weight_decay) || !std::isfinite(hp->grad_scale))
+        return DISDP_ERR_INVALID_ARG;
+    return DISDP_OK;
+}
+
+// The step constants: 1 - beta^t and 1 - lr*wd in double, rounded once.
+disdp::StepScalars step_scalars(const disdp_adamw_hparams_t *hp)
+{
+    disdp::StepScalars s;
+    s.b1 = hp->beta1;
+    s.omb1 = 1.0f - hp->beta1;
+    s.b2 = hp->beta2;
+    s.omb2 = 1.0f - hp->beta2;
+    const double t = static_cast<double>(hp->step);
+    s.bc1 = static_cast<float>(1.0 - std::pow(static_cast<double>(hp->beta1), t));
+    s.bc2 = static_cast<float>(1.0 - std::pow(static_cast<double>(hp->beta2), t));
+    s.decay = static_cast<float>(1.0 - static_cast<double>(hp->lr) *
+                                           static_cast<double>(hp->weight_decay));
+    s.lr = hp->lr;
+    s.eps = hp->eps;
+    s.grad_scale = hp->grad_scale;
+    return s;
+}
+
+bool aligned(const void *p, uintptr_t a)
+{
+    return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0;
+}
+
+// Shared body of the three entry points.  `adam` selects the optimizer;
+// for disdp_adam_step the single contribution is the fp32 aggregate itself
+// (an aggregate of one fp32 contribution is that contribution, unrounded).
+disdp_status_t run(const void *const *grads, int W, int gdtype, int64_t n,
+                   int mode, int frac_bits, float *param, float *m, float *v,
+                   uint16_t *p16, float *agg_f32, int32_t *agg_i32,
+                   const disdp_adamw_hparams_t *hp, bool adam,
+                   bool agg_f32_required, hipStream_t stream)
+{
+    disdp_status_t st = check_counts(W, gdtype, n, mode, frac_bits);
+    if (st != DISDP_OK)
+        return st;
+    if (adam && (st = check_hparams(hp)) != DISDP_OK)
+        return st;
+    if (mode == DISDP_AGG_FP32 && agg_i32)
+        return DISDP_ERR_INVALID_ARG;  // an int32 aggregate exists only in fixed mode
+    if (n == 0)
+        return DISDP_OK;
+
+    // NULL pointers
+    if (!grads)
+        return DISDP_ERR_INVALID_ARG;
+    for (int w = 0; w < W; ++w)
+        if (!grads[w])
+            return DISDP_ERR_INVALID_ARG;
+    if (adam && (!param || !m || !v))
+        return DISDP_ERR_INVALID_ARG;
+    if (!adam) {
+        if (agg_f32_required && !agg_f32)
+            return DISDP_ERR_INVALID_ARG;
+        if (!agg_f32 && !agg_i32)
+            return DISDP_ERR_INVALID_ARG;
+    }
+
+    // Overlap: every output against every other buffer.
+    const int gb = grad_bytes(gdtype);
+    Span outs[6];
+    int nout = 0;
+    if (param) outs[nout++] = span_of(param, n, 4);
+    if (m) outs[nout++] = span_of(m, n, 4);
+    if (v) outs[nout++] = span_of(v, n, 4);
+    if (p16) outs[nout++] = span_of(p16, n, 2);
+    if (agg_f32) outs[nout++] = span_of(agg_f32, n, 4);
+    if (agg_i32) outs[nout++] = span_of(agg_i32, n, 4);
+    for (int i = 0; i < nout; ++i) {
+        for (int j = i + 1; j < nout; ++j)
+            if (overlaps(outs[i], outs[j]))
+                return DISDP_ERR_ALIAS;
+        for (int w = 0; w < W; ++w)
+            if (overlaps(outs[i], span_of(grads[w], n, gb)))
+                return DISDP_ERR_ALIAS;
+    }
+
+    LaunchArgs a;
+    std::memset(&a, 0, sizeof a);
+    for (int w = 0; w < W; ++w)
+        a.g[w] = grads[w];
+    a.p = param;
+    a.m = m;
+    a.v = v;
+    a.p16 = p16;
+    a.agg_f32 = agg_f32;
+    a.agg_i32 = agg_i32;
+    a.n = n;
+    a.W = W;
+    a.gdtype = gdtype;
+    a.mode = mode;
+    a.frac_bits = (mode == DISDP_AGG_FIXED) ? frac_bits : 0;
+    a.qscale = std::ldexp(1.0f, a.frac_bits);
+    a.dqscale = std::ldexp(1.0f, -a.frac_bits);
+    if (adam)
+        a.s = step_scalars(hp);
+
+    // Vector kernels move 4 elements per lane: 16-byte fp32 groups and
+    // 8-byte bf16 groups.
+    bool vec = true;
+    for (int w = 0; w < W; ++w)
+        vec = vec && aligned(grads[w], gdtype == DISDP_DT_BF16 ? 8 : 16);
+    for (const void *p : {static_cast<const void *>(param), static_cast<const void *>(m),
+                          static_cast<const void *>(v), static_cast<const void *>(agg_f32),
+                          static_cast<const void *>(agg_i32)})
+        vec = vec && aligned(p, 16);
+    vec = vec && aligned(p16, 8);
+
+    hipError_t e = disdp::launch(a, adam ? disdp::kAggregateAdam : disdp::kAggregateOnly,
+                                 vec, stream);
+    return e == hipSuccess ? DISDP_OK : DISDP_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+disdp_status_t disdp_aggregate(const void *const *grads, int W, disdp_dtype_t gdtype,
+                               int64_t n, disdp_agg_mode_t mode, int frac_bits,
+                               float *agg_out_f32, int32_t *agg_out_i32,
+                               hipStream_t stream)
+{
+    return run(grads, W, gdtype, n, mode, frac_bits, nullptr, nullptr, nullptr,
+               nullptr, agg_out_f32, agg_out_i32, nullptr, /*adam=*/false,
+               /*agg_f32_required=*/mode == DISDP_AGG_FP32, stream);
+}
+
+disdp_status_t disdp_adam_step(const float *grad, float *param, float *m, float *v,
+                               uint16_t *param_bf16_out, int64_t n,
+                               const disdp_adamw_hparams_t *hp, hipStream_t stream)
+{
+    const void *grads[1] = {grad};
+    return run(grads, 1, DISDP_DT_F32, n, DISDP_AGG_FP32, 0, param, m, v,
+               param_bf16_out, nullptr, nullptr, hp, /*adam=*/true,
+               /*agg_f32_required=*/false, stream);
+}
+
+disdp_status_t disdp_aggregate_adam(const void *const *grads, int W,
+                                    disdp_dtype_t gdtype, int64_t n,
+                                    disdp_agg_mode_t mode, int frac_bits,
+                                    float *param, float *m, float *v,
+                                    uint16_t *param_bf16_out, float *agg_out_f32,
+                                    int32_t *agg_out_i32,
+                                    const disdp_adamw_hparams_t *hp,
+                                    hipStream_t stream)
+{
+    return run(grads, W, gdtype, n, mode, frac_bits, param, m, v, param_bf16_out,
+               agg_out_f32, agg_out_i32, hp, /*adam=*/true,
+               /*agg_f32_required=*/false, stream);
+}
+
+const char *disdp_status_string(disdp_status_t status)
+{
+    switch (status) {
+    case DISDP_OK: return "ok";
+    case DISDP_ERR_INVALID_ARG: return "invalid argument";
+    case DISDP_ERR_UNSUPPORTED: return "unsupported dtype or mode";
+    case DISDP_ERR_ALIAS: return "output overlaps another buffer";
+    case DISDP_ERR_HIP: return "HIP launch failed";
+    }
+    return "unknown status";
+}
+
+}  // extern "C"

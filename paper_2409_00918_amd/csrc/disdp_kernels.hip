@@ -1,0 +1,432 @@
+// gfx950 kernels of libdisdp: the W-way reduction of a shard's gradient
+// contributions (the SmartSwitch's aggregation in DisDP, Sections III-A and
+// III-C, in fp32 or in the integer format of Section III-B), optionally
+// fused with the parameter server's mixed-precision Adam step and its bf16
+// parameter copy (Section III-D, step 5).
+//
+// The path is a pure HBM stream: per element it reads W contributions and
+// 12 bytes of state and writes 12 bytes of state and 2 bytes of copy, with
+// a few dozen ALU operations in between.  No MFMA: there is no contraction.
+// Design for CDNA4:
+//   * one lane owns 4 consecutive elements, so every stream moves in 16-byte
+//     (fp32) or 8-byte (bf16) vector accesses and each wave instruction
+//     covers 1 KiB / 512 B of contiguous memory;
+//   * a block owns a tile of kBlock * U groups; all loads of a tile (W
+//     contributions and p, m, v for U groups) are issued before any
+//     arithmetic so each wave keeps U * (W + 3) vector loads in flight;
+//   * tiles are distributed grid-stride over a grid sized to the chip, so
+//     every byte is read once and written once;
+//   * data are touched once, so loads and stores carry the non-temporal hint;
+//   * no atomics, no cross-lane traffic: each element's reduction is one
+//     lane's serial chain in worker order, which makes results independent
+//     of grid size and identical to an element-wise evaluation.
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <cstdint>
+
+#include "disdp_launch.h"
+
+// One rounding per written operation: never contract a*b+c into an FMA.
+#pragma clang fp contract(off)
+
+namespace disdp {
+namespace {
+
+constexpr int kBlock = 256;
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+
+template <typename T>
+__device__ __forceinline__ T ld_nt(const T *p)
+{
+    return __builtin_nontemporal_load(p);
+}
+
+template <typename T>
+__device__ __forceinline__ void st_nt(T *p, T v)
+{
+    __builtin_nontemporal_store(v, p);
+}
+
+// ---- element operations ---------------------------------------------------
+
+// bf16 bits -> fp32: the bf16 pattern is the upper half of the fp32 one.
+__device__ __forceinline__ float widen_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float widen_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// fp32 -> bf16 bits, round to nearest even; NaN -> quiet NaN with its sign.
+__device__ __forceinline__ uint32_t to_bf16(float x)
+{
+    const uint32_t u = __float_as_uint(x);
+    const uint32_t rounded = (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+    const uint32_t qnan = ((u >> 16) & 0x8000u) | 0x7fc0u;
+    return (u & 0x7fffffffu) > 0x7f800000u ? qnan : rounded;
+}
+
+// Contribution -> int32 at scale 2^k: exact scaling, rint (ties to even),
+// saturation, NaN -> 0.
+__device__ __forceinline__ int32_t quantize(float x, float scale)
+{
+    const float y = x * scale;
+    if (__builtin_isnan(y))
+        return 0;
+    const float r = __builtin_rintf(y);
+    if (r >= 2147483648.0f)
+        return INT32_MAX;
+    if (r < -2147483648.0f)
+        return INT32_MIN;
+    return static_cast<int32_t>(r);
+}
+
+__device__ __forceinline__ int32_t saturate32(int64_t s)
+{
+    return s > INT32_MAX ? INT32_MAX : (s < INT32_MIN ? INT32_MIN : static_cast<int32_t>(s));
+}
+
+// One AdamW step on one element (decoupled decay, bias-corrected moments,
+// eps outside the square root).  `/` and sqrtf are the correctly rounded
+// IEEE operations on this target.
+__device__ __forceinline__ void adamw(const StepScalars &s, float agg, float &p, float &m,
+                                      float &v)
+{
+    const float g = agg * s.grad_scale;
+    const float mi = s.b1 * m + s.omb1 * g;
+    const float vi = s.b2 * v + s.omb2 * (g * g);
+    const float mh = mi / s.bc1;
+    const float vh = vi / s.bc2;
+    const float d = sqrtf(vh) + s.eps;
+    p = p * s.decay - s.lr * (mh / d);
+    m = mi;
+    v = vi;
+}
+
+// ---- loading contributions -----------------------------------------------
+
+// Four consecutive elements of contribution `base` at group index `grp`.
+template <int GT>
+__device__ __forceinline__ void load_group(const void *base, int64_t grp, float (&x)[4])
+{
+    if constexpr (GT == kGradF32) {
+        const f32x4 v = ld_nt(reinterpret_cast<const f32x4 *>(base) + grp);
+        x[0] = v.x;
+        x[1] = v.y;
+        x[2] = v.z;
+        x[3] = v.w;
+    } else {
+        const u32x2 h = ld_nt(reinterpret_cast<const u32x2 *>(base) + grp);
+        x[0] = widen_lo(h.x);
+        x[1] = widen_hi(h.x);
+        x[2] = widen_lo(h.y);
+        x[3] = widen_hi(h.y);
+    }
+}
+
+template <int GT>
+__device__ __forceinline__ float load_one(const void *base, int64_t i)
+{
+    if constexpr (GT == kGradF32)
+        return reinterpret_cast<const float *>(base)[i];
+    else
+        return widen_lo(reinterpret_cast<const uint16_t *>(base)[i]);
+}
+
+// ---- the reduction of one element over its W contributions ----------------
+
+// Accumulator of one element: fp32 running sum, or exact 64-bit integer sum.
+template <int MODE>
+struct Acc {
+    float f;
+    int64_t s;
+    __device__ __forceinline__ void first(float x, float qscale)
+    {
+        if constexpr (MODE == kAggFP32)
+            f = x;
+        else
+            s = quantize(x, qscale);
+    }
+    __device__ __forceinline__ void next(float x, float qscale)
+    {
+        if constexpr (MODE == kAggFP32)
+            f = f + x;
+        else
+            s += quantize(x, qscale);
+    }
+    // (fp32 aggregate, int32 aggregate)
+    __device__ __forceinline__ float result(float dqscale, int32_t &ai) const
+    {
+        if constexpr (MODE == kAggFP32) {
+            ai = 0;
+            return f;
+        } else {
+            ai = saturate32(s);
+            return static_cast<float>(ai) * dqscale;
+        }
+    }
+};
+
+// ---- writing one group's results -----------------------------------------
+
+template <int MODE, bool ADAM>
+__device__ __forceinline__ void finish_group(const LaunchArgs &a, int64_t grp, const float (&agg)[4],
+                                             const int32_t (&ai)[4], f32x4 P, f32x4 M, f32x4 V)
+{
+    if (a.agg_f32)
+        st_nt(reinterpret_cast<f32x4 *>(a.agg_f32) + grp, f32x4{agg[0], agg[1], agg[2], agg[3]});
+    if constexpr (MODE == kAggFixed) {
+        if (a.agg_i32)
+            st_nt(reinterpret_cast<i32x4 *>(a.agg_i32) + grp, i32x4{ai[0], ai[1], ai[2], ai[3]});
+    }
+    if constexpr (ADAM) {
+        float p[4] = {P.x, P.y, P.z, P.w};
+        float m[4] = {M.x, M.y, M.z, M.w};
+        float v[4] = {V.x, V.y, V.z, V.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            adamw(a.s, agg[e], p[e], m[e], v[e]);
+        st_nt(reinterpret_cast<f32x4 *>(a.p) + grp, f32x4{p[0], p[1], p[2], p[3]});
+        st_nt(reinterpret_cast<f32x4 *>(a.m) + grp, f32x4{m[0], m[1], m[2], m[3]});
+        st_nt(reinterpret_cast<f32x4 *>(a.v) + grp, f32x4{v[0], v[1], v[2], v[3]});
+        if (a.p16)
+            st_nt(reinterpret_cast<u32x2 *>(a.p16) + grp,
+                  u32x2{to_bf16(p[0]) | (to_bf16(p[1]) << 16),
+                        to_bf16(p[2]) | (to_bf16(p[3]) << 16)});
+    }
+}
+
+// ---- U groups per lane, W known at compile time ---------------------------
+
+// Groups g0, g0 + kBlock, ..., g0 + (U-1) kBlock: every load first, then
+// the arithmetic, then the stores.
+template <int W, int GT, int MODE, bool ADAM, int U>
+__device__ __forceinline__ void process_groups(const LaunchArgs &a, int64_t g0)
+{
+    float c[U][W][4];
+    f32x4 P[U], M[U], V[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+#pragma unroll
+        for (int w = 0; w < W; ++w)
+            load_group<GT>(a.g[w], g0 + u * kBlock, c[u][w]);
+        if constexpr (ADAM) {
+            P[u] = ld_nt(reinterpret_cast<const f32x4 *>(a.p) + g0 + u * kBlock);
+            M[u] = ld_nt(reinterpret_cast<const f32x4 *>(a.m) + g0 + u * kBlock);
+            V[u] = ld_nt(reinterpret_cast<const f32x4 *>(a.v) + g0 + u * kBlock);
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        float agg[4];
+        int32_t ai[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            Acc<MODE> acc;
+            acc.first(c[u][0][e], a.qscale);
+#pragma unroll
+            for (int w = 1; w < W; ++w)
+                acc.next(c[u][w][e], a.qscale);
+            agg[e] = acc.result(a.dqscale, ai[e]);
+        }
+        finish_group<MODE, ADAM>(a, g0 + u * kBlock, agg, ai, P[u], M[u], V[u]);
+    }
+}
+
+// ---- one group per lane, W known only at run time (W <= 64) ---------------
+
+// Contributions are read in chunks of 8 (all 8 loads in flight, then the
+// eight additions in worker order).
+template <int GT, int MODE, bool ADAM>
+__device__ __forceinline__ void process_group_rt(const LaunchArgs &a, int64_t grp)
+{
+    constexpr int kChunk = 8;
+    f32x4 P{}, M{}, V{};
+    if constexpr (ADAM) {
+        P = ld_nt(reinterpret_cast<const f32x4 *>(a.p) + grp);
+        M = ld_nt(reinterpret_cast<const f32x4 *>(a.m) + grp);
+        V = ld_nt(reinterpret_cast<const f32x4 *>(a.v) + grp);
+    }
+    Acc<MODE> acc[4];
+    for (int w0 = 0; w0 < a.W; w0 += kChunk) {
+        float c[kChunk][4];
+#pragma unroll
+        for (int j = 0; j < kChunk; ++j)
+            if (w0 + j < a.W)
+                load_group<GT>(a.g[w0 + j], grp, c[j]);
+#pragma unroll
+        for (int j = 0; j < kChunk; ++j) {
+            if (w0 + j < a.W) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    if (w0 + j == 0)
+                        acc[e].first(c[j][e], a.qscale);
+                    else
+                        acc[e].next(c[j][e], a.qscale);
+                }
+            }
+        }
+    }
+    float agg[4];
+    int32_t ai[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+        agg[e] = acc[e].result(a.dqscale, ai[e]);
+    finish_group<MODE, ADAM>(a, grp, agg, ai, P, M, V);
+}
+
+// ---- one element -----------------------------------------------------------
+
+template <int GT, int MODE, bool ADAM>
+__device__ __forceinline__ void process_element(const LaunchArgs &a, int64_t i)
+{
+    Acc<MODE> acc;
+    acc.first(load_one<GT>(a.g[0], i), a.qscale);
+    for (int w = 1; w < a.W; ++w)
+        acc.next(load_one<GT>(a.g[w], i), a.qscale);
+    int32_t ai;
+    const float agg = acc.result(a.dqscale, ai);
+    if (a.agg_f32)
+        a.agg_f32[i] = agg;
+    if constexpr (MODE == kAggFixed) {
+        if (a.agg_i32)
+            a.agg_i32[i] = ai;
+    }
+    if constexpr (ADAM) {
+        float p = a.p[i], m = a.m[i], v = a.v[i];
+        adamw(a.s, agg, p, m, v);
+        a.p[i] = p;
+        a.m[i] = m;
+        a.v[i] = v;
+        if (a.p16)
+            a.p16[i] = static_cast<uint16_t>(to_bf16(p));
+    }
+}
+
+// ---- kernels -----------------------------------------------------------------
+
+// Vector kernel.  W > 0: compile-time worker count, U groups per lane;
+// W == 0: run-time worker count, one group per lane.  Groups [0, n/4) go
+// grid-stride in tiles of kBlock*U groups; the groups after the last full
+// tile go one per lane; the last n % 4 elements go to lanes of block 0.
+template <int W, int GT, int MODE, bool ADAM, int U>
+__global__ __launch_bounds__(kBlock) void vector_kernel(LaunchArgs a)
+{
+    const int64_t n_groups = a.n >> 2;
+    const int64_t tile = static_cast<int64_t>(kBlock) * U;
+    const int64_t n_tiles = n_groups / tile;
+    for (int64_t t = blockIdx.x; t < n_tiles; t += gridDim.x) {
+        const int64_t g0 = t * tile + threadIdx.x;
+        if constexpr (W > 0)
+            process_groups<W, GT, MODE, ADAM, U>(a, g0);
+        else
+            process_group_rt<GT, MODE, ADAM>(a, g0);
+    }
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+    for (int64_t grp = n_tiles * tile + static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+         grp < n_groups; grp += stride) {
+        if constexpr (W > 0)
+            process_groups<W, GT, MODE, ADAM, 1>(a, grp);
+        else
+            process_group_rt<GT, MODE, ADAM>(a, grp);
+    }
+    if (blockIdx.x == 0 && threadIdx.x < (a.n & 3))
+        process_element<GT, MODE, ADAM>(a, (n_groups << 2) + threadIdx.x);
+}
+
+// Element-wise kernel for buffers that are not vector aligned.
+template <int GT, int MODE, bool ADAM>
+__global__ __launch_bounds__(kBlock) void element_kernel(LaunchArgs a)
+{
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < a.n; i += stride)
+        process_element<GT, MODE, ADAM>(a, i);
+}
+
+// ---- host side: grid sizing and dispatch --------------------------------------
+
+// Resident blocks per CU the grid aims for; the grid-stride loop covers
+// the rest of the shard.
+constexpr int kBlocksPerCU = 8;
+constexpr int kU = 2;
+
+int cu_count()
+{
+    static std::atomic<int> cached[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64)
+        return 256;
+    int c = cached[dev].load(std::memory_order_relaxed);
+    if (c <= 0) {
+        if (hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            c <= 0)
+            c = 256;
+        cached[dev].store(c, std::memory_order_relaxed);
+    }
+    return c;
+}
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+hipError_t launch_kernel(const void *fn, int64_t blocks, const LaunchArgs &a, hipStream_t stream)
+{
+    const int64_t cap = static_cast<int64_t>(cu_count()) * kBlocksPerCU;
+    if (blocks > cap)
+        blocks = cap;
+    if (blocks < 1)
+        blocks = 1;
+    void *args[] = {const_cast<LaunchArgs *>(&a)};
+    return hipLaunchKernel(fn, dim3(static_cast<unsigned>(blocks)), dim3(kBlock), args, 0, stream);
+}
+
+template <int W, int GT, int MODE, bool ADAM>
+hipError_t launch_vector(const LaunchArgs &a, hipStream_t stream)
+{
+    constexpr int U = W > 0 ? kU : 1;
+    const int64_t n_groups = a.n >> 2;
+    const int64_t blocks = ceil_div(n_groups, static_cast<int64_t>(kBlock) * U);
+    return launch_kernel(reinterpret_cast<const void *>(&vector_kernel<W, GT, MODE, ADAM, U>),
+                         blocks, a, stream);
+}
+
+template <int GT, int MODE, bool ADAM>
+hipError_t dispatch_w(const LaunchArgs &a, bool vec, hipStream_t stream)
+{
+    if (!vec)
+        return launch_kernel(reinterpret_cast<const void *>(&element_kernel<GT, MODE, ADAM>),
+                             ceil_div(a.n, kBlock), a, stream);
+    switch (a.W) {
+    case 1: return launch_vector<1, GT, MODE, ADAM>(a, stream);
+    case 2: return launch_vector<2, GT, MODE, ADAM>(a, stream);
+    case 3: return launch_vector<3, GT, MODE, ADAM>(a, stream);
+    case 4: return launch_vector<4, GT, MODE, ADAM>(a, stream);
+    case 5: return launch_vector<5, GT, MODE, ADAM>(a, stream);
+    case 6: return launch_vector<6, GT, MODE, ADAM>(a, stream);
+    case 7: return launch_vector<7, GT, MODE, ADAM>(a, stream);
+    case 8: return launch_vector<8, GT, MODE, ADAM>(a, stream);
+    case 12: return launch_vector<12, GT, MODE, ADAM>(a, stream);
+    case 16: return launch_vector<16, GT, MODE, ADAM>(a, stream);
+    default: return launch_vector<0, GT, MODE, ADAM>(a, stream);
+    }
+}
+
+template <bool ADAM>
+hipError_t dispatch(const LaunchArgs &a, bool vec, hipStream_t stream)
+{
+    if (a.gdtype == kGradF32)
+        return a.mode == kAggFP32 ? dispatch_w<kGradF32, kAggFP32, ADAM>(a, vec, stream)
+                                  : dispatch_w<kGradF32, kAggFixed, ADAM>(a, vec, stream);
+    return a.mode == kAggFP32 ? dispatch_w<kGradBF16, kAggFP32, ADAM>(a, vec, stream)
+                              : dispatch_w<kGradBF16, kAggFixed, ADAM>(a, vec, stream);
+}
+
+}  // namespace
+
+hipError_t launch(const LaunchArgs &a, Kind kind, bool vector_path, hipStream_t stream)
+{
+    return kind == kAggregateAdam ? dispatch<true>(a, vector_path, stream)
+                                  : dispatch<false>(a, vector_path, stream);
+}
+
+}  // namespace disdp

@@ -1,0 +1,43 @@
+// Internal interface between the C-ABI front end (disdp_api.cpp) and the
+// gfx950 kernels (disdp_kernels.hip).  Not installed; not part of the ABI.
+#pragma once
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+namespace disdp {
+
+constexpr int kMaxW = 64;
+
+enum GradType { kGradF32 = 0, kGradBF16 = 1 };
+enum AggMode { kAggFP32 = 0, kAggFixed = 1 };
+enum Kind { kAggregateOnly = 0, kAggregateAdam = 1 };
+
+// Per-step constants of the optimizer, evaluated once on the host.
+struct StepScalars {
+    float b1, omb1;   // beta1, 1 - beta1
+    float b2, omb2;   // beta2, 1 - beta2
+    float bc1, bc2;   // 1 - beta1^t, 1 - beta2^t
+    float decay;      // 1 - lr * weight_decay
+    float lr, eps, grad_scale;
+};
+
+// Everything a kernel needs, passed by value in the kernel-argument segment.
+struct LaunchArgs {
+    const void *g[kMaxW];  // W contribution pointers (device)
+    float *p, *m, *v;      // in-place state (device), NULL in aggregate-only
+    uint16_t *p16;         // bf16 parameter copy, may be NULL
+    float *agg_f32;        // optional fp32 aggregate
+    int32_t *agg_i32;      // optional int32 aggregate (fixed mode)
+    int64_t n;
+    int W, gdtype, mode, frac_bits;
+    float qscale, dqscale; // 2^k and 2^-k (fixed mode)
+    StepScalars s;
+};
+
+// Enqueues the kernel for `a` on `stream`.  `vector_path` selects the
+// 4-elements-per-lane kernels (all pointers suitably aligned).
+hipError_t launch(const LaunchArgs &a, Kind kind, bool vector_path,
+                  hipStream_t stream);
+
+}  // namespace disdp

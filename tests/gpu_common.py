@@ -1,0 +1,133 @@
+"""Shared helpers of the GPU parity tests (not a test module).
+
+Inputs come from ``synth`` (seeded), are uploaded to the device, run through
+the C ABI (via the thin binding) and the results are compared element by
+element with the CPU oracle run on the same input bits.
+"""
+import numpy as np
+
+import oracle
+import synth
+
+HP = dict(lr=np.float32(1e-4), beta1=np.float32(0.9), beta2=np.float32(0.95),
+          eps=np.float32(1e-8), wd=np.float32(0.1))
+
+
+def torch():
+    import torch as _t
+    return _t
+
+
+def to_dev(a: np.ndarray, offset: int = 0):
+    """Device copy of `a`; with offset > 0 the tensor starts `offset`
+    elements into a larger allocation (an unaligned pointer)."""
+    t = torch()
+    if a.dtype == np.uint16:
+        a = a.view(np.int16)
+    src = t.from_numpy(np.ascontiguousarray(a))
+    if offset == 0:
+        return src.cuda()
+    big = t.zeros(a.size + offset + 8, dtype=src.dtype, device="cuda")
+    big[offset:offset + a.size].copy_(src)
+    return big[offset:offset + a.size]
+
+
+def to_host(x) -> np.ndarray:
+    t = torch()
+    a = x.detach().cpu().numpy()
+    if x.dtype == t.int16:
+        a = a.view(np.uint16)
+    return a
+
+
+def bits(a):
+    return np.ascontiguousarray(a, dtype=np.float32).view(np.uint32)
+
+
+def f32_same(a, b) -> bool:
+    """Bit-identical, except that any NaN matches any NaN."""
+    a = np.asarray(a, np.float32)
+    b = np.asarray(b, np.float32)
+    na, nb = np.isnan(a), np.isnan(b)
+    return bool(np.array_equal(na, nb) and np.array_equal(bits(a[~na]), bits(b[~nb])))
+
+
+def bf16_same(a, b) -> bool:
+    a = np.asarray(a, np.uint16)
+    b = np.asarray(b, np.uint16)
+    na = (a & 0x7FFF) > 0x7F80
+    nb = (b & 0x7FFF) > 0x7F80
+    return bool(np.array_equal(na, nb) and np.array_equal(a[~na], b[~nb]))
+
+
+def max_rel_err(got, want) -> float:
+    got = np.asarray(got, np.float64)
+    want = np.asarray(want, np.float64)
+    ok = np.isfinite(want) & np.isfinite(got)
+    if not ok.any():
+        return 0.0
+    d = np.abs(got[ok] - want[ok])
+    den = np.abs(want[ok])
+    rel = np.where(den > 0, d / np.where(den > 0, den, 1.0), np.where(d > 0, np.inf, 0.0))
+    return float(rel.max())
+
+
+def bf16_ulp_diff(a, b) -> int:
+    """Largest distance in bf16 units in the last place between finite
+    patterns (ordered as sign-magnitude integers)."""
+    def key(h):
+        h = np.asarray(h, np.int64)
+        return np.where(h & 0x8000, -(h & 0x7FFF), h & 0x7FFF)
+    fin = ((np.asarray(a) & 0x7FFF) < 0x7F80) & ((np.asarray(b) & 0x7FFF) < 0x7F80)
+    if not fin.any():
+        return 0
+    return int(np.max(np.abs(key(a)[fin] - key(b)[fin])))
+
+
+def assert_parity(got: dict, want: dict, label: str) -> None:
+    """Bit parity of every output present in both dicts, plus the stated
+    tolerances (max relative error 1e-6 for fp32 state, 1 bf16 ulp)."""
+    for k in ("agg_i32",):
+        if k in want and k in got:
+            assert np.array_equal(got[k], want[k]), f"{label}: {k} differs"
+    for k in ("agg_f32", "p", "m", "v"):
+        if k in want and k in got:
+            assert max_rel_err(got[k], want[k]) <= 1e-6, f"{label}: {k} rel err"
+            assert f32_same(got[k], want[k]), f"{label}: {k} not bit-identical"
+    if "p16" in want and "p16" in got:
+        assert bf16_ulp_diff(got["p16"], want["p16"]) <= 1, f"{label}: p16 ulp"
+        assert bf16_same(got["p16"], want["p16"]), f"{label}: p16 not bit-identical"
+
+
+def run_fused_case(W, gdtype, mode, n, t=3, frac_bits=24, offsets=(0, 0),
+                   want_agg=True, want_p16=True, seed=0, sigma=1e-4, hp=None):
+    """One disdp_aggregate_adam call against the oracle.  offsets[0] shifts
+    the contributions, offsets[1] the state and outputs."""
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    hp = dict(HP if hp is None else hp)
+    gs = synth.host_grads(100 + seed, t, W, n, sigma, gdtype=gdtype,
+                          outlier_frac=0.01, outlier_scale=100.0)
+    p, m, v = synth.host_state(100 + seed, n, mv_sigma=sigma)
+    dg = [to_dev(g, offsets[0]) for g in gs]
+    dp, dm, dv = (to_dev(x, offsets[1]) for x in (p, m, v))
+    d16 = to_dev(np.zeros(n, np.uint16), offsets[1]) if want_p16 else None
+    daf = to_dev(np.zeros(n, np.float32), offsets[1]) if want_agg else None
+    dai = to_dev(np.zeros(n, np.int32), offsets[1]) if (want_agg and mode == "fixed") else None
+    dd.aggregate_adam(dg, dp, dm, dv, d16, lr=hp["lr"], beta1=hp["beta1"],
+                      beta2=hp["beta2"], eps=hp["eps"], weight_decay=hp["wd"],
+                      step=t, mode=mode, frac_bits=frac_bits, agg_out_f32=daf,
+                      agg_out_i32=dai)
+    t_.cuda.synchronize()
+    got = {"p": to_host(dp), "m": to_host(dm), "v": to_host(dv)}
+    if want_p16:
+        got["p16"] = to_host(d16)
+    if daf is not None:
+        got["agg_f32"] = to_host(daf)
+    if dai is not None:
+        got["agg_i32"] = to_host(dai)
+    want = oracle.fused(gs, p, m, v, mode=oracle.AGG_FIXED if mode == "fixed" else oracle.AGG_FP32,
+                        frac_bits=frac_bits, t=t, want_bf16=want_p16,
+                        want_agg_f32=want_agg, want_agg_i32=(want_agg and mode == "fixed"),
+                        **hp)
+    return got, want

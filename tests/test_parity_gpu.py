@@ -1,0 +1,349 @@
+"""GPU parity of libdisdp against the CPU oracle, at sizes the oracle finishes
+in seconds: every entry point, both gradient types, both aggregation modes,
+compile-time and run-time worker counts, ragged lengths around the tile and
+vector boundaries, unaligned pointers, special values, the tiny-shard
+workload over 10 steps, and the equivalences the ABI promises.
+
+The bar is bit parity with the oracle (integer aggregates, fp32 state and
+the bf16 copy); the stated tolerances (fp32 relative error <= 1e-6, bf16
+within 1 ulp) are asserted as well.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from gpu_common import (HP, assert_parity, bits, f32_same, run_fused_case,
+                        to_dev, to_host, torch)
+
+pytestmark = pytest.mark.gpu
+
+# lengths: empty-ish, below one vector group, around 4-element groups,
+# around one wave / block / tile (256 lanes, 2 groups per lane), and larger
+# ragged shards spanning many tiles
+LENGTHS = [1, 2, 3, 4, 5, 7, 8, 9, 63, 255, 256, 257, 1023, 1024, 1025, 2047,
+           2048, 2049, 2051, 4099, 65541, 300_007]
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    import paper_2409_00918_amd as dd
+    dd.lib()
+    t = torch()
+    assert t.cuda.is_available(), "GPU tests need a device"
+
+
+def _label(**kw):
+    return " ".join(f"{k}={v}" for k, v in kw.items())
+
+
+@pytest.mark.parametrize("W", [1, 2, 3, 4, 8, 16])
+@pytest.mark.parametrize("gdtype", ["f32", "bf16"])
+@pytest.mark.parametrize("mode", ["fp32", "fixed"])
+def test_fused_sweep_lengths(W, gdtype, mode):
+    for i, n in enumerate(LENGTHS):
+        got, want = run_fused_case(W, gdtype, mode, n, t=1 + i % 5, seed=i)
+        assert_parity(got, want, _label(W=W, gdtype=gdtype, mode=mode, n=n))
+
+
+@pytest.mark.parametrize("W", [5, 9, 13, 33, 64])
+@pytest.mark.parametrize("gdtype,mode", [("f32", "fp32"), ("bf16", "fixed"),
+                                         ("f32", "fixed"), ("bf16", "fp32")])
+def test_fused_runtime_worker_counts(W, gdtype, mode):
+    for i, n in enumerate([3, 1029, 70_001]):
+        got, want = run_fused_case(W, gdtype, mode, n, t=2 + i, seed=50 + i)
+        assert_parity(got, want, _label(W=W, gdtype=gdtype, mode=mode, n=n))
+
+
+@pytest.mark.parametrize("offsets", [(1, 0), (0, 1), (2, 3), (3, 2)])
+@pytest.mark.parametrize("gdtype,mode", [("f32", "fp32"), ("bf16", "fixed")])
+def test_fused_unaligned_pointers(offsets, gdtype, mode):
+    for n in (1, 6, 1000, 40_001):
+        got, want = run_fused_case(8, gdtype, mode, n, t=4, offsets=offsets, seed=7)
+        assert_parity(got, want, _label(offsets=offsets, n=n))
+
+
+@pytest.mark.parametrize("want_agg,want_p16", [(False, False), (True, False), (False, True)])
+def test_fused_optional_outputs(want_agg, want_p16):
+    for mode in ("fp32", "fixed"):
+        got, want = run_fused_case(4, "f32", mode, 10_007, t=5, want_agg=want_agg,
+                                   want_p16=want_p16, seed=3)
+        assert_parity(got, want, _label(mode=mode))
+
+
+@pytest.mark.parametrize("frac_bits", [0, 8, 16, 30])
+def test_fused_fixed_scales(frac_bits):
+    # at 2^30 a 1e-4 * 100 outlier reaches ~1e8, and contributions of 3e1
+    # saturate; at 2^0 most contributions quantise to 0
+    got, want = run_fused_case(8, "f32", "fixed", 50_001, t=2, frac_bits=frac_bits,
+                               sigma=3.0 if frac_bits == 30 else 1e-4, seed=9)
+    assert_parity(got, want, _label(frac_bits=frac_bits))
+
+
+def test_fused_hyperparameter_variants():
+    variants = [dict(HP, lr=np.float32(3e-4)), dict(HP, wd=np.float32(0.0)),
+                dict(HP, beta1=np.float32(0.0), beta2=np.float32(0.0)),
+                dict(HP, beta2=np.float32(0.999), eps=np.float32(1e-6)),
+                dict(HP, eps=np.float32(0.0))]
+    for i, hp in enumerate(variants):
+        for t in (1, 7, 1000):
+            got, want = run_fused_case(3, "bf16", "fp32", 5003, t=t, hp=hp, seed=20 + i)
+            assert_parity(got, want, _label(variant=i, t=t))
+
+
+# ------------------------------------------------------------- special values --
+def _special_contributions(n, W):
+    rng = np.random.default_rng(5)
+    pool = np.array([0.0, -0.0, 1e-45, -1e-45, 1e-40, -3e-39, 1.1754942e-38, 5e-8,
+                     -5e-8, 2.0**-25, 3 * 2.0**-25, 1e3, -1e3, 65504.0, 3e38, -3e38,
+                     np.inf, -np.inf, np.nan, 127.99999, -128.0, 128.0],
+                    dtype=np.float32)
+    return [pool[rng.integers(0, pool.size, n)] for _ in range(W)]
+
+
+@pytest.mark.parametrize("mode", ["fp32", "fixed"])
+def test_fused_special_values(mode):
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    n, W = 4099, 4
+    gs = _special_contributions(n, W)
+    p, m, v = synth.host_state(77, n, mv_sigma=1e-3)
+    p[:50] = np.float32(1e-42)          # denormal weights
+    m[50:100] = np.float32(-1e-41)
+    v[100:150] = np.float32(1e-44)      # denormal second moments
+    dg = [to_dev(g) for g in gs]
+    dp, dm, dv = to_dev(p), to_dev(m), to_dev(v)
+    d16 = to_dev(np.zeros(n, np.uint16))
+    daf = to_dev(np.zeros(n, np.float32))
+    dai = to_dev(np.zeros(n, np.int32)) if mode == "fixed" else None
+    dd.aggregate_adam(dg, dp, dm, dv, d16, lr=HP["lr"], beta1=HP["beta1"],
+                      beta2=HP["beta2"], eps=HP["eps"], weight_decay=HP["wd"],
+                      step=3, mode=mode, frac_bits=24, agg_out_f32=daf, agg_out_i32=dai)
+    t_.cuda.synchronize()
+    want = oracle.fused(gs, p, m, v, mode=oracle.AGG_FIXED if mode == "fixed" else oracle.AGG_FP32,
+                        frac_bits=24, t=3, want_agg_f32=True,
+                        want_agg_i32=(mode == "fixed"), **HP)
+    got = {"p": to_host(dp), "m": to_host(dm), "v": to_host(dv), "p16": to_host(d16),
+           "agg_f32": to_host(daf)}
+    if dai is not None:
+        got["agg_i32"] = to_host(dai)
+    assert_parity(got, want, f"special values, {mode}")
+
+
+def test_adam_step_division_and_sqrt_across_magnitudes():
+    # gradients spread over the whole fp32 range (incl. denormals) stress the
+    # correctly rounded divide and square root
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    rng = np.random.default_rng(123)
+    n = 200_003
+    e = rng.integers(-149, 60, n).astype(np.float64)
+    g = (rng.choice([-1.0, 1.0], n) * rng.uniform(1, 2, n) * 2.0**e).astype(np.float32)
+    p = rng.standard_normal(n).astype(np.float32)
+    m = (rng.standard_normal(n) * 2.0**rng.integers(-140, 30, n)).astype(np.float32)
+    v = np.abs(rng.standard_normal(n) * 2.0**rng.integers(-149, 60, n)).astype(np.float32)
+    for t in (1, 2, 17):
+        dg, dp, dm, dv = to_dev(g), to_dev(p), to_dev(m), to_dev(v)
+        d16 = to_dev(np.zeros(n, np.uint16))
+        dd.adam_step(dg, dp, dm, dv, d16, lr=HP["lr"], beta1=HP["beta1"], beta2=HP["beta2"],
+                     eps=HP["eps"], weight_decay=HP["wd"], step=t)
+        t_.cuda.synchronize()
+        p1, m1, v1, p16 = oracle.adamw(g, p, m, v, t=t, **HP)
+        assert_parity({"p": to_host(dp), "m": to_host(dm), "v": to_host(dv), "p16": to_host(d16)},
+                      {"p": p1, "m": m1, "v": v1, "p16": p16}, f"t={t}")
+
+
+# ----------------------------------------------------------- the three calls --
+@pytest.mark.parametrize("W,gdtype,mode", [(8, "f32", "fp32"), (16, "bf16", "fp32"),
+                                           (8, "f32", "fixed"), (5, "bf16", "fixed"),
+                                           (1, "f32", "fp32")])
+def test_aggregate_matches_oracle(W, gdtype, mode):
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    for n in (1, 5, 1027, 123_457):
+        gs = synth.host_grads(300 + W, 1, W, n, 1e-4, gdtype=gdtype, outlier_frac=0.01,
+                              outlier_scale=1e4)
+        dg = [to_dev(g) for g in gs]
+        daf = to_dev(np.zeros(n, np.float32))
+        dai = to_dev(np.zeros(n, np.int32)) if mode == "fixed" else None
+        dd.aggregate(dg, mode=mode, frac_bits=24, agg_out_f32=daf, agg_out_i32=dai)
+        t_.cuda.synchronize()
+        if mode == "fixed":
+            ai, af = oracle.aggregate_fixed(gs, 24)
+            assert np.array_equal(to_host(dai), ai), n
+        else:
+            af = oracle.aggregate_f32(gs)
+        assert f32_same(to_host(daf), af), n
+
+
+def test_aggregate_fixed_int_only_output():
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    n = 9001
+    gs = synth.host_grads(310, 0, 3, n, 1e-4)
+    dai = to_dev(np.zeros(n, np.int32))
+    dd.aggregate([to_dev(g) for g in gs], mode="fixed", frac_bits=20, agg_out_i32=dai)
+    t_.cuda.synchronize()
+    assert np.array_equal(to_host(dai), oracle.aggregate_fixed(gs, 20)[0])
+
+
+def test_aggregate_fixed_is_worker_order_independent_on_device():
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    n, W = 33_333, 8
+    gs = synth.host_grads(311, 0, W, n, 1e-3, outlier_frac=0.05, outlier_scale=1e6)
+    dg = [to_dev(g) for g in gs]
+    outs = []
+    for perm in (list(range(W)), list(reversed(range(W))), [3, 1, 7, 0, 2, 6, 4, 5]):
+        dai = to_dev(np.zeros(n, np.int32))
+        daf = to_dev(np.zeros(n, np.float32))
+        dd.aggregate([dg[j] for j in perm], mode="fixed", frac_bits=24,
+                     agg_out_f32=daf, agg_out_i32=dai)
+        t_.cuda.synchronize()
+        outs.append((to_host(dai), bits(to_host(daf))))
+    for o in outs[1:]:
+        assert np.array_equal(o[0], outs[0][0]) and np.array_equal(o[1], outs[0][1])
+
+
+def test_adam_step_matches_oracle():
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    for n in (1, 3, 4, 1025, 250_001):
+        g = synth.host_grads(320, 0, 1, n, 1e-3, outlier_frac=0.01, outlier_scale=100.0)[0]
+        p, m, v = synth.host_state(320, n, mv_sigma=1e-3)
+        dg, dp, dm, dv = to_dev(g), to_dev(p), to_dev(m), to_dev(v)
+        d16 = to_dev(np.zeros(n, np.uint16))
+        dd.adam_step(dg, dp, dm, dv, d16, lr=HP["lr"], beta1=HP["beta1"], beta2=HP["beta2"],
+                     eps=HP["eps"], weight_decay=HP["wd"], step=6)
+        t_.cuda.synchronize()
+        p1, m1, v1, p16 = oracle.adamw(g, p, m, v, t=6, **HP)
+        assert_parity({"p": to_host(dp), "m": to_host(dm), "v": to_host(dv), "p16": to_host(d16)},
+                      {"p": p1, "m": m1, "v": v1, "p16": p16}, f"n={n}")
+
+
+@pytest.mark.parametrize("W,gdtype,mode", [(8, "f32", "fp32"), (16, "bf16", "fp32"),
+                                           (8, "f32", "fixed"), (7, "bf16", "fixed")])
+def test_fused_equals_aggregate_then_adam_step(W, gdtype, mode):
+    """The ABI promise: the fused call is bit-identical to the two-call path."""
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    n = 100_003
+    gs = synth.host_grads(330, 0, W, n, 1e-4, gdtype=gdtype)
+    p, m, v = synth.host_state(330, n, mv_sigma=1e-4)
+    dg = [to_dev(g) for g in gs]
+    kw = dict(lr=HP["lr"], beta1=HP["beta1"], beta2=HP["beta2"], eps=HP["eps"],
+              weight_decay=HP["wd"], step=3)
+    a = [to_dev(x) for x in (p, m, v)] + [to_dev(np.zeros(n, np.uint16))]
+    dd.aggregate_adam(dg, *a, mode=mode, frac_bits=24, **kw)
+    b = [to_dev(x) for x in (p, m, v)] + [to_dev(np.zeros(n, np.uint16))]
+    agg = to_dev(np.zeros(n, np.float32))
+    dd.aggregate(dg, mode=mode, frac_bits=24, agg_out_f32=agg)
+    dd.adam_step(agg, *b, **kw)
+    t_.cuda.synchronize()
+    for x, y in zip(a, b):
+        assert np.array_equal(to_host(x), to_host(y))
+
+
+def test_empty_shard_writes_nothing():
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    e = t_.empty(0, device="cuda")
+    dd.aggregate([e, e], agg_out_f32=e)
+    dd.adam_step(e, t_.empty(0, device="cuda"), t_.empty(0, device="cuda"),
+                 t_.empty(0, device="cuda"), lr=1e-4, beta1=0.9, beta2=0.95, eps=1e-8,
+                 weight_decay=0.1, step=1)
+    t_.cuda.synchronize()
+
+
+def test_errors_are_raised_by_the_binding_on_device():
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    x = t_.zeros(16, device="cuda")
+    with pytest.raises(dd.DisdpError) as ei:
+        dd.aggregate([x, x], agg_out_f32=x)          # output is an input
+    assert ei.value.status == dd.ERR_ALIAS
+    with pytest.raises(dd.DisdpError) as ei:
+        dd.adam_step(t_.zeros(16, device="cuda"), x, t_.zeros(16, device="cuda"),
+                     t_.zeros(16, device="cuda"), lr=1e-4, beta1=1.0, beta2=0.95,
+                     eps=1e-8, weight_decay=0.1, step=1)
+    assert ei.value.status == dd.ERR_INVALID_ARG
+
+
+# --------------------------------------------------------- streams and state --
+def test_side_stream_and_determinism():
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    n, W = 1_000_003, 8
+    gs = synth.host_grads(340, 0, W, n, 1e-4)
+    p, m, v = synth.host_state(340, n, mv_sigma=1e-4)
+    dg = [to_dev(g) for g in gs]
+    res = []
+    s = t_.cuda.Stream()
+    for use_side in (False, True):
+        st = [to_dev(x) for x in (p, m, v)] + [to_dev(np.zeros(n, np.uint16))]
+        t_.cuda.synchronize()
+        if use_side:
+            with t_.cuda.stream(s):
+                dd.aggregate_adam(dg, *st, lr=HP["lr"], beta1=HP["beta1"], beta2=HP["beta2"],
+                                  eps=HP["eps"], weight_decay=HP["wd"], step=2)
+            s.synchronize()
+        else:
+            dd.aggregate_adam(dg, *st, lr=HP["lr"], beta1=HP["beta1"], beta2=HP["beta2"],
+                              eps=HP["eps"], weight_decay=HP["wd"], step=2)
+            t_.cuda.synchronize()
+        res.append([to_host(x) for x in st])
+    for x, y in zip(*res):
+        assert np.array_equal(x, y)
+
+
+def test_resume_from_saved_state_is_bit_identical():
+    """5 steps straight equal 2 steps, a save/restore of (p, m, v, t), and 3
+    more steps: all optimizer state is the caller's."""
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    n, W = 20_011, 4
+    p, m, v = synth.host_state(350, n)
+    grads = [[to_dev(g) for g in synth.host_grads(350, t, W, n, 1e-3)] for t in range(1, 6)]
+    kw = dict(lr=HP["lr"], beta1=HP["beta1"], beta2=HP["beta2"], eps=HP["eps"],
+              weight_decay=HP["wd"])
+
+    def steps(state, ts):
+        for t in ts:
+            dd.aggregate_adam(grads[t - 1], *state, step=t, **kw)
+        t_.cuda.synchronize()
+
+    a = [to_dev(x) for x in (p, m, v)] + [to_dev(np.zeros(n, np.uint16))]
+    steps(a, range(1, 6))
+    b = [to_dev(x) for x in (p, m, v)] + [to_dev(np.zeros(n, np.uint16))]
+    steps(b, range(1, 3))
+    saved = [to_host(x) for x in b]
+    c = [to_dev(x) for x in saved]
+    steps(c, range(3, 6))
+    for x, y in zip(a, c):
+        assert np.array_equal(to_host(x), to_host(y))
+
+
+# -------------------------------------------------- tiny shard, 10 steps ------
+def test_tiny_shard_ten_steps_against_oracle():
+    """N = 1,048,576, W = 4 fp32 contributions ~ N(0, 1e-3), weights
+    ~ N(0, 0.02), m = v = 0, AdamW(1e-4, 0.9, 0.95, 1e-8, 0.1), fresh seeded
+    gradients each of 10 steps, bf16 copy out; every element every step."""
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    wl = synth.WORKLOADS["tiny_n1M_w4_f32"]
+    n, W = wl.n, wl.W
+    p, m, v = synth.host_state(wl.wid, n, wl.p_sigma)
+    dp, dm, dv = to_dev(p), to_dev(m), to_dev(v)
+    d16 = to_dev(np.zeros(n, np.uint16))
+    hp = dict(lr=np.float32(wl.lr), beta1=np.float32(wl.beta1), beta2=np.float32(wl.beta2),
+              eps=np.float32(wl.eps), wd=np.float32(wl.wd))
+    for t in range(1, wl.steps + 1):
+        gs = synth.host_grads(wl.wid, t, W, n, wl.sigma)
+        dd.aggregate_adam([to_dev(g) for g in gs], dp, dm, dv, d16, lr=hp["lr"],
+                          beta1=hp["beta1"], beta2=hp["beta2"], eps=hp["eps"],
+                          weight_decay=hp["wd"], step=t)
+        t_.cuda.synchronize()
+        want = oracle.fused(gs, p, m, v, t=t, **hp)
+        got = {"p": to_host(dp), "m": to_host(dm), "v": to_host(dv), "p16": to_host(d16)}
+        assert_parity(got, want, f"step {t}")
+        p, m, v = want["p"], want["m"], want["v"]
