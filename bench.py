@@ -12,6 +12,7 @@ lr 1e-4, betas (0.9, 0.95), eps 1e-8, weight decay 0.1.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME]
     python bench.py --interference      # fused call next to a bf16 GEMM loop
+    python bench.py --copy-probe        # plain 4 GiB device copy (counter scale)
 
 Prints one JSON line.  ``roofline`` prices the kernel against HBM bandwidth
 (8 TB/s) with algorithmic bytes (each byte the call must move, counted once);
@@ -48,8 +49,9 @@ KERNEL_SOURCES = ["paper_2409_00918_amd/csrc/disdp_kernels.hip",
                   "paper_2409_00918_amd/csrc/disdp_launch.h",
                   "paper_2409_00918_amd/csrc/disdp_api.cpp",
                   "paper_2409_00918_amd/build.py"]
-CPU_SAMPLE = 1 << 25            # elements of the shard the oracle is timed on
-CPU_STEPS = 4
+CPU_SAMPLE = 1 << 26            # elements of the shard the oracle is timed on
+CPU_STEPS = 12
+COPY_PROBE_ELEMS = 1 << 30      # fp32 elements moved by the copy probe (4 GiB each way)
 
 
 def kernel_source_hash() -> str:
@@ -92,6 +94,30 @@ def allocate(wl):
     dp, dm, dv = synth.device_state(wl.wid, wl.n, wl.p_sigma)
     d16 = torch.empty(wl.n, dtype=torch.int16, device="cuda")
     return dg, dp, dm, dv, d16
+
+
+def copy_ceiling_gbps(elems=1 << 30, reps=10):
+    """Bytes moved per second by a plain device copy (torch's copy kernel)
+    of `elems` fp32 elements on this GPU, measured now: the practical HBM
+    ceiling the fused kernel is compared with, next to the datasheet peak."""
+    import numpy as np
+    import torch
+    src = torch.ones(elems, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    s = torch.cuda.current_stream()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(reps)]
+    for a, b in ev:
+        a.record(s)
+        dst.copy_(src)
+        b.record(s)
+    torch.cuda.synchronize()
+    ms = float(np.median([a.elapsed_time(b) for a, b in ev]))
+    del src, dst
+    torch.cuda.empty_cache()
+    return round(2 * elems * 4 / (ms * 1e-3) / 1e9, 1)
 
 
 def cpu_baseline(wl, dg, dp, dm, dv):
@@ -166,6 +192,8 @@ def run_bench(args):
     avg_kernel_ms = float(np.mean(kernel_ms))
     ms_per_step = wall * 1e3 / args.steps
 
+    copy_gbps = None if args.no_copy_ceiling else copy_ceiling_gbps()
+
     gb = 2 if wl.gdtype == "bf16" else 4
     bpe = dd.algorithmic_bytes_per_element(wl.W, gb)
     algo_bytes = wl.n * bpe
@@ -180,7 +208,9 @@ def run_bench(args):
                 "algorithmic_bytes_per_element": bpe,
                 "avg_kernel_ms": round(avg_kernel_ms, 4),
                 "min_kernel_ms": round(float(np.min(kernel_ms)), 4),
-                "kernel_source_hash": src_hash}
+                "kernel_source_hash": src_hash,
+                "copy_ceiling_GBps": copy_gbps,
+                "frac_of_copy_ceiling": None if not copy_gbps else round(achieved / copy_gbps, 4)}
     value = wl.n / (ms_per_step * 1e-3) / 1e9
     line = {
         "metric": "G params/s aggregated+updated (fused W-way reduction + AdamW + bf16 copy)",
@@ -291,6 +321,35 @@ def run_interference(args):
     print(json.dumps(line), flush=True)
 
 
+def run_copy_probe(args):
+    """A plain device-to-device copy of COPY_PROBE_ELEMS fp32 elements
+    (torch's elementwise copy kernel): known bytes read and written per
+    launch, against which the HBM byte counters of the fused kernel are
+    scaled."""
+    import numpy as np
+    import torch
+    torch.cuda.set_device(0)
+    src = torch.ones(COPY_PROBE_ELEMS, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(args.warmup):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    s = torch.cuda.current_stream()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    for a, b in ev:
+        a.record(s)
+        dst.copy_(src)
+        b.record(s)
+    torch.cuda.synchronize()
+    ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    nbytes = COPY_PROBE_ELEMS * 4
+    print(json.dumps({"metric": "copy probe", "bytes_read_per_launch": nbytes,
+                      "bytes_written_per_launch": nbytes, "avg_ms": round(ms, 4),
+                      "GBps": round(2 * nbytes / (ms * 1e-3) / 1e9, 1),
+                      "launches": args.steps}), flush=True)
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -298,7 +357,9 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-copy-ceiling", action="store_true")
     ap.add_argument("--interference", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true")
     args = ap.parse_args(argv)
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus > 1 or world > 1:
@@ -308,6 +369,8 @@ def main(argv=None):
         return 2
     if args.interference:
         run_interference(args)
+    elif args.copy_probe:
+        run_copy_probe(args)
     else:
         run_bench(args)
     return 0

@@ -14,8 +14,9 @@
 //   * a block owns a tile of kBlock * U groups; all loads of a tile (W
 //     contributions and p, m, v for U groups) are issued before any
 //     arithmetic so each wave keeps U * (W + 3) vector loads in flight;
-//   * tiles are distributed grid-stride over a grid sized to the chip, so
-//     every byte is read once and written once;
+//   * one tile per block over a grid that covers the shard (a persistent,
+//     occupancy-sized grid is a compile-time alternative), so every byte is
+//     read once and written once;
 //   * data are touched once, so loads and stores carry the non-temporal hint;
 //   * no atomics, no cross-lane traffic: each element's reduction is one
 //     lane's serial chain in worker order, which makes results independent
@@ -24,16 +25,73 @@
 
 #include <atomic>
 #include <cstdint>
+#include <mutex>
 
 #include "disdp_launch.h"
 
 // One rounding per written operation: never contract a*b+c into an FMA.
 #pragma clang fp contract(off)
 
+// Launch-shape tunables (compile-time).  The defaults -- one 256-lane tile
+// per block, one group per lane, non-temporal loads and stores, tiles in
+// natural order -- were the best or tied-best in interleaved A/B runs on
+// MI355X over the 7B/8, 13B/16 and 175B/64 shards; the other settings were
+// within 2% or slower (persistent grids, more groups per lane, wider blocks,
+// wave-contiguous groups, XCD-chunked tile orders, hints on one side only).
+//   DISDP_UNROLL      groups of 4 elements per lane per tile (loads in flight)
+//   DISDP_GRID_MODE   0: persistent grid of (resident blocks per CU) x CUs x
+//                        DISDP_GRID_ROUNDS blocks, tiles grid-stride;
+//                     1: one tile per block
+//   DISDP_NT          non-temporal hints on loads (bit 0) and stores (bit 1)
+//   DISDP_BLOCK       lanes per block
+//   DISDP_WAVE_CONTIG 1: a wave's U groups are contiguous (U KiB per fp32
+//                     stream per wave); 0: strided by the block width
+//   DISDP_MIN_WAVES   launch-bounds hint: waves per SIMD to fit (0 = none)
+//   DISDP_XCD_CHUNK   0: block b takes tile b.  C > 0 (one tile per block):
+//                     the dispatcher deals blocks round-robin to the 8
+//                     XCDs, and XCD x takes the chunks x, x+8, x+16, ... of
+//                     C consecutive tiles, its blocks walking them in order.
+//                     -1: C = ceil(tiles / 8), one contiguous eighth of the
+//                     shard per XCD.
+#ifndef DISDP_UNROLL
+#define DISDP_UNROLL 1
+#endif
+#ifndef DISDP_GRID_MODE
+#define DISDP_GRID_MODE 1
+#endif
+#ifndef DISDP_GRID_ROUNDS
+#define DISDP_GRID_ROUNDS 1
+#endif
+#ifndef DISDP_NT
+#define DISDP_NT 3
+#endif
+#ifndef DISDP_BLOCK
+#define DISDP_BLOCK 256
+#endif
+#ifndef DISDP_WAVE_CONTIG
+#define DISDP_WAVE_CONTIG 0
+#endif
+#ifndef DISDP_MIN_WAVES
+#define DISDP_MIN_WAVES 0
+#endif
+#ifndef DISDP_XCD_CHUNK
+#define DISDP_XCD_CHUNK 0
+#endif
+#if DISDP_XCD_CHUNK != 0 && DISDP_GRID_MODE != 1
+#error "DISDP_XCD_CHUNK needs one tile per block (DISDP_GRID_MODE=1)"
+#endif
+constexpr int kXcds = 8;
+#if DISDP_MIN_WAVES > 0
+#define DISDP_LAUNCH_BOUNDS __launch_bounds__(DISDP_BLOCK, DISDP_MIN_WAVES)
+#else
+#define DISDP_LAUNCH_BOUNDS __launch_bounds__(DISDP_BLOCK)
+#endif
+
 namespace disdp {
 namespace {
 
-constexpr int kBlock = 256;
+constexpr int kBlock = DISDP_BLOCK;
+constexpr int kWave = 64;
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
@@ -43,13 +101,21 @@ typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 template <typename T>
 __device__ __forceinline__ T ld_nt(const T *p)
 {
+#if DISDP_NT & 1
     return __builtin_nontemporal_load(p);
+#else
+    return *p;
+#endif
 }
 
 template <typename T>
 __device__ __forceinline__ void st_nt(T *p, T v)
 {
+#if DISDP_NT & 2
     __builtin_nontemporal_store(v, p);
+#else
+    *p = v;
+#endif
 }
 
 // ---- element operations ---------------------------------------------------
@@ -199,10 +265,10 @@ __device__ __forceinline__ void finish_group(const LaunchArgs &a, int64_t grp, c
 
 // ---- U groups per lane, W known at compile time ---------------------------
 
-// Groups g0, g0 + kBlock, ..., g0 + (U-1) kBlock: every load first, then
+// Groups g0, g0 + stride, ..., g0 + (U-1) stride: every load first, then
 // the arithmetic, then the stores.
 template <int W, int GT, int MODE, bool ADAM, int U>
-__device__ __forceinline__ void process_groups(const LaunchArgs &a, int64_t g0)
+__device__ __forceinline__ void process_groups(const LaunchArgs &a, int64_t g0, int stride)
 {
     float c[U][W][4];
     f32x4 P[U], M[U], V[U];
@@ -210,11 +276,11 @@ __device__ __forceinline__ void process_groups(const LaunchArgs &a, int64_t g0)
     for (int u = 0; u < U; ++u) {
 #pragma unroll
         for (int w = 0; w < W; ++w)
-            load_group<GT>(a.g[w], g0 + u * kBlock, c[u][w]);
+            load_group<GT>(a.g[w], g0 + u * stride, c[u][w]);
         if constexpr (ADAM) {
-            P[u] = ld_nt(reinterpret_cast<const f32x4 *>(a.p) + g0 + u * kBlock);
-            M[u] = ld_nt(reinterpret_cast<const f32x4 *>(a.m) + g0 + u * kBlock);
-            V[u] = ld_nt(reinterpret_cast<const f32x4 *>(a.v) + g0 + u * kBlock);
+            P[u] = ld_nt(reinterpret_cast<const f32x4 *>(a.p) + g0 + u * stride);
+            M[u] = ld_nt(reinterpret_cast<const f32x4 *>(a.m) + g0 + u * stride);
+            V[u] = ld_nt(reinterpret_cast<const f32x4 *>(a.v) + g0 + u * stride);
         }
     }
 #pragma unroll
@@ -230,7 +296,7 @@ __device__ __forceinline__ void process_groups(const LaunchArgs &a, int64_t g0)
                 acc.next(c[u][w][e], a.qscale);
             agg[e] = acc.result(a.dqscale, ai[e]);
         }
-        finish_group<MODE, ADAM>(a, g0 + u * kBlock, agg, ai, P[u], M[u], V[u]);
+        finish_group<MODE, ADAM>(a, g0 + u * stride, agg, ai, P[u], M[u], V[u]);
     }
 }
 
@@ -306,20 +372,47 @@ __device__ __forceinline__ void process_element(const LaunchArgs &a, int64_t i)
 
 // ---- kernels -----------------------------------------------------------------
 
+// Tiles per XCD chunk for a shard of `n_tiles` full tiles (>= 1).
+__host__ __device__ __forceinline__ int64_t xcd_chunk(int64_t n_tiles)
+{
+    if (DISDP_XCD_CHUNK > 0)
+        return DISDP_XCD_CHUNK;
+    const int64_t c = (n_tiles + kXcds - 1) / kXcds;
+    return c > 0 ? c : 1;
+}
+
 // Vector kernel.  W > 0: compile-time worker count, U groups per lane;
 // W == 0: run-time worker count, one group per lane.  Groups [0, n/4) go
 // grid-stride in tiles of kBlock*U groups; the groups after the last full
 // tile go one per lane; the last n % 4 elements go to lanes of block 0.
 template <int W, int GT, int MODE, bool ADAM, int U>
-__global__ __launch_bounds__(kBlock) void vector_kernel(LaunchArgs a)
+__global__ DISDP_LAUNCH_BOUNDS void vector_kernel(LaunchArgs a)
 {
     const int64_t n_groups = a.n >> 2;
     const int64_t tile = static_cast<int64_t>(kBlock) * U;
     const int64_t n_tiles = n_groups / tile;
+#if DISDP_WAVE_CONTIG
+    const int lane_off = (threadIdx.x / kWave) * (kWave * U) + threadIdx.x % kWave;
+    constexpr int kStride = kWave;
+#else
+    const int lane_off = threadIdx.x;
+    constexpr int kStride = kBlock;
+#endif
+#if DISDP_XCD_CHUNK != 0
+    // one tile per block; block b is the j-th block of XCD x = b mod 8, and
+    // XCD x's j-th tile is tile j mod C of its (j / C)-th chunk, which is
+    // chunk (j / C) * 8 + x of the shard
+    const int64_t chunk = xcd_chunk(n_tiles);
+    const int64_t j = blockIdx.x / kXcds;
+    const int64_t t_first = ((j / chunk) * kXcds + blockIdx.x % kXcds) * chunk + j % chunk;
+    const int64_t t_end = t_first < n_tiles ? t_first + 1 : 0;
+    for (int64_t t = t_first; t < t_end; ++t) {
+#else
     for (int64_t t = blockIdx.x; t < n_tiles; t += gridDim.x) {
-        const int64_t g0 = t * tile + threadIdx.x;
+#endif
+        const int64_t g0 = t * tile + lane_off;
         if constexpr (W > 0)
-            process_groups<W, GT, MODE, ADAM, U>(a, g0);
+            process_groups<W, GT, MODE, ADAM, U>(a, g0, kStride);
         else
             process_group_rt<GT, MODE, ADAM>(a, g0);
     }
@@ -327,7 +420,7 @@ __global__ __launch_bounds__(kBlock) void vector_kernel(LaunchArgs a)
     for (int64_t grp = n_tiles * tile + static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
          grp < n_groups; grp += stride) {
         if constexpr (W > 0)
-            process_groups<W, GT, MODE, ADAM, 1>(a, grp);
+            process_groups<W, GT, MODE, ADAM, 1>(a, grp, kBlock);
         else
             process_group_rt<GT, MODE, ADAM>(a, grp);
     }
@@ -337,7 +430,7 @@ __global__ __launch_bounds__(kBlock) void vector_kernel(LaunchArgs a)
 
 // Element-wise kernel for buffers that are not vector aligned.
 template <int GT, int MODE, bool ADAM>
-__global__ __launch_bounds__(kBlock) void element_kernel(LaunchArgs a)
+__global__ DISDP_LAUNCH_BOUNDS void element_kernel(LaunchArgs a)
 {
     const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
     for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < a.n; i += stride)
@@ -346,10 +439,7 @@ __global__ __launch_bounds__(kBlock) void element_kernel(LaunchArgs a)
 
 // ---- host side: grid sizing and dispatch --------------------------------------
 
-// Resident blocks per CU the grid aims for; the grid-stride loop covers
-// the rest of the shard.
-constexpr int kBlocksPerCU = 8;
-constexpr int kU = 2;
+constexpr int kU = DISDP_UNROLL;
 
 int cu_count()
 {
@@ -367,13 +457,46 @@ int cu_count()
     return c;
 }
 
+// Blocks of `fn` that fit on one CU at once (registers decide it here),
+// cached per kernel.  Occupancy depends only on the kernel and the block
+// size, so one entry per kernel serves every device of one architecture.
+int resident_blocks_per_cu(const void *fn)
+{
+    static std::mutex mu;
+    static const void *keys[512];
+    static int vals[512];
+    static int used = 0;
+    std::lock_guard<std::mutex> lock(mu);
+    for (int i = 0; i < used; ++i)
+        if (keys[i] == fn)
+            return vals[i];
+    int nb = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, fn, kBlock, 0) != hipSuccess || nb < 1)
+        nb = 1;
+    if (used < 512) {
+        keys[used] = fn;
+        vals[used] = nb;
+        ++used;
+    }
+    return nb;
+}
+
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-hipError_t launch_kernel(const void *fn, int64_t blocks, const LaunchArgs &a, hipStream_t stream)
+// `work_blocks`: blocks needed for one tile (or element chunk) each.
+hipError_t launch_kernel(const void *fn, int64_t work_blocks, bool persistent, const LaunchArgs &a,
+                         hipStream_t stream)
 {
-    const int64_t cap = static_cast<int64_t>(cu_count()) * kBlocksPerCU;
-    if (blocks > cap)
-        blocks = cap;
+    int64_t blocks = work_blocks;
+    if (persistent) {
+        const int64_t cap = static_cast<int64_t>(cu_count()) * resident_blocks_per_cu(fn) *
+                            DISDP_GRID_ROUNDS;
+        if (blocks > cap)
+            blocks = cap;
+    }
+    // one-tile-per-block grids stay within the 32-bit grid limit
+    if (blocks > 0x7fffffff)
+        blocks = 0x7fffffff;
     if (blocks < 1)
         blocks = 1;
     void *args[] = {const_cast<LaunchArgs *>(&a)};
@@ -385,9 +508,18 @@ hipError_t launch_vector(const LaunchArgs &a, hipStream_t stream)
 {
     constexpr int U = W > 0 ? kU : 1;
     const int64_t n_groups = a.n >> 2;
-    const int64_t blocks = ceil_div(n_groups, static_cast<int64_t>(kBlock) * U);
+    int64_t blocks = ceil_div(n_groups, static_cast<int64_t>(kBlock) * U);
+#if DISDP_XCD_CHUNK != 0
+    // every XCD gets ceil(chunks / 8) chunks of C blocks; the ragged groups
+    // after the last full tile go to the grid-stride loop of all blocks
+    {
+        const int64_t n_tiles = n_groups / (static_cast<int64_t>(kBlock) * U);
+        const int64_t c = xcd_chunk(n_tiles);
+        blocks = kXcds * ceil_div(ceil_div(n_tiles, c), kXcds) * c;
+    }
+#endif
     return launch_kernel(reinterpret_cast<const void *>(&vector_kernel<W, GT, MODE, ADAM, U>),
-                         blocks, a, stream);
+                         blocks, DISDP_GRID_MODE == 0, a, stream);
 }
 
 template <int GT, int MODE, bool ADAM>
@@ -395,7 +527,7 @@ hipError_t dispatch_w(const LaunchArgs &a, bool vec, hipStream_t stream)
 {
     if (!vec)
         return launch_kernel(reinterpret_cast<const void *>(&element_kernel<GT, MODE, ADAM>),
-                             ceil_div(a.n, kBlock), a, stream);
+                             ceil_div(a.n, kBlock), /*persistent=*/true, a, stream);
     switch (a.W) {
     case 1: return launch_vector<1, GT, MODE, ADAM>(a, stream);
     case 2: return launch_vector<2, GT, MODE, ADAM>(a, stream);
