@@ -47,19 +47,35 @@ HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, published peak
 DEFAULT_WORKLOAD = "opt7b_shard8_w8_f32"
 KERNEL_SOURCES = ["paper_2409_00918_amd/csrc/disdp_kernels.hip",
                   "paper_2409_00918_amd/csrc/disdp_launch.h",
-                  "paper_2409_00918_amd/csrc/disdp_api.cpp",
-                  "paper_2409_00918_amd/build.py"]
+                  "paper_2409_00918_amd/csrc/disdp_api.cpp"]
 CPU_SAMPLE = 1 << 26            # elements of the shard the oracle is timed on
 CPU_STEPS = 12
 COPY_PROBE_ELEMS = 1 << 30      # fp32 elements moved by the copy probe (4 GiB each way)
 
 
 def kernel_source_hash() -> str:
+    """Hash of what decides the fused kernel's machine code: its sources and
+    the compile flags of libdisdp."""
+    from paper_2409_00918_amd import build as _build
     h = hashlib.sha256()
     for rel in KERNEL_SOURCES:
         with open(os.path.join(ROOT, rel), "rb") as f:
             h.update(f.read())
+    h.update(" ".join(a for a in _build.FLAGS if not a.startswith("/")).encode())
     return h.hexdigest()[:16]
+
+
+def probe_lib():
+    """libdisdp_probe.so (a plain copy kernel), loaded after torch so that it
+    binds to torch's HIP runtime."""
+    import ctypes
+    import torch  # noqa: F401
+    from paper_2409_00918_amd import build as _build
+    L = ctypes.CDLL(_build.PROBE_LIB)
+    L.disdp_probe_copy.restype = ctypes.c_int
+    L.disdp_probe_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                   ctypes.c_void_p]
+    return L
 
 
 def committed_traffic(workload: str, src_hash: str):
@@ -97,21 +113,23 @@ def allocate(wl):
 
 
 def copy_ceiling_gbps(elems=1 << 30, reps=10):
-    """Bytes moved per second by a plain device copy (torch's copy kernel)
-    of `elems` fp32 elements on this GPU, measured now: the practical HBM
-    ceiling the fused kernel is compared with, next to the datasheet peak."""
+    """Bytes moved per second by a plain copy kernel (16-byte non-temporal
+    loads and stores, libdisdp_probe.so) of `elems` fp32 elements on this
+    GPU, measured now: the practical HBM ceiling the fused kernel is
+    compared with, next to the datasheet peak."""
     import numpy as np
     import torch
+    L = probe_lib()
     src = torch.ones(elems, device="cuda")
     dst = torch.empty_like(src)
-    dst.copy_(src)
-    torch.cuda.synchronize()
     s = torch.cuda.current_stream()
+    assert L.disdp_probe_copy(src.data_ptr(), dst.data_ptr(), elems * 4, s.cuda_stream or None) == 0
+    torch.cuda.synchronize()
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(reps)]
     for a, b in ev:
         a.record(s)
-        dst.copy_(src)
+        L.disdp_probe_copy(src.data_ptr(), dst.data_ptr(), elems * 4, s.cuda_stream or None)
         b.record(s)
     torch.cuda.synchronize()
     ms = float(np.median([a.elapsed_time(b) for a, b in ev]))
@@ -239,11 +257,32 @@ def run_bench(args):
     print(json.dumps(line), flush=True)
 
 
+def _cu_mask_stream(first_cu: int, count: int, total: int):
+    """A default-priority stream restricted to CUs [first_cu, first_cu+count)
+    (hipExtStreamCreateWithCUMask on torch's HIP runtime), wrapped for torch."""
+    import ctypes
+    import torch
+    hip = ctypes.CDLL("libamdhip64.so.7")      # torch's runtime, already loaded
+    words = (total + 31) // 32
+    mask = (ctypes.c_uint32 * words)()
+    for cu in range(first_cu, first_cu + count):
+        mask[cu // 32] |= 1 << (cu % 32)
+    handle = ctypes.c_void_p()
+    rc = hip.hipExtStreamCreateWithCUMask(ctypes.byref(handle), ctypes.c_uint32(words), mask)
+    if rc != 0:
+        raise RuntimeError(f"hipExtStreamCreateWithCUMask failed ({rc})")
+    return torch.cuda.ExternalStream(handle.value), handle, hip
+
+
 def run_interference(args):
-    """The fused call for the 7B / 8 shard on a side stream next to a compute
-    stream looping a bf16 GEMM M = N = K = 8192 (seeded N(0, 1) inputs); the
-    slowdown of each against its solo time.  torch.matmul is the vendor GEMM,
-    used only as the antagonist."""
+    """The fused call for the 7B / 8 shard on one stream next to a stream
+    looping a bf16 GEMM M = N = K = 8192 (seeded N(0, 1) inputs).  Every
+    kernel is bracketed by events measured from one common origin, so the
+    overlap is observed, not assumed: `gemm_busy_frac` is the share of the
+    fused calls' time window during which a GEMM was executing.  With
+    --cu-split K the fused call runs on a stream masked to K CUs and the GEMM
+    on a stream masked to the other CUs (K = 0: both streams unmasked).
+    torch.matmul is the vendor GEMM, the antagonist only."""
     import numpy as np
     import torch
     import paper_2409_00918_amd as dd
@@ -259,92 +298,115 @@ def run_interference(args):
     A = torch.randn(8192, 8192, generator=gen, device="cuda").to(torch.bfloat16)
     B = torch.randn(8192, 8192, generator=gen, device="cuda").to(torch.bfloat16)
     C = torch.empty(8192, 8192, device="cuda", dtype=torch.bfloat16)
-    side = torch.cuda.Stream()
-    comp = torch.cuda.Stream()
+    n_cu = torch.cuda.get_device_properties(0).multi_processor_count
     t_state = [0]
+    med = lambda x: float(np.median(x)) if len(x) else None
 
-    def fused_on(stream):
+    def fused(stream):
         t_state[0] += 1
         dd.aggregate_adam(dg, dp, dm, dv, d16, lr=hp["lr"], beta1=hp["beta1"],
                           beta2=hp["beta2"], eps=hp["eps"], weight_decay=hp["wd"],
                           step=t_state[0], stream=stream)
 
-    def timed(stream, fn, reps):
-        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-              for _ in range(reps)]
+    def gemm(stream):
         with torch.cuda.stream(stream):
-            for s, e in ev:
-                s.record(stream)
-                fn(stream)
-                e.record(stream)
+            torch.matmul(A, B, out=C)
+
+    def enqueue(stream, fn, reps):
+        ev = []
+        for _ in range(reps):
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            fn(stream)
+            b.record(stream)
+            ev.append((a, b))
         return ev
 
-    def gemm(stream):
-        torch.matmul(A, B, out=C)
+    def spans(origin, ev):
+        return [(origin.elapsed_time(a), origin.elapsed_time(b)) for a, b in ev]
 
-    reps_f = args.steps
-    # warm both up
-    for _ in range(2):
-        fused_on(side)
-        with torch.cuda.stream(comp):
+    for k in [int(x) for x in args.cu_split.split(",")]:
+        handles = []
+        if k == 0:
+            side, comp = torch.cuda.Stream(), torch.cuda.Stream()
+        else:
+            side, h1, hip = _cu_mask_stream(0, k, n_cu)
+            comp, h2, _ = _cu_mask_stream(k, n_cu - k, n_cu)
+            handles = [(hip, h1), (hip, h2)]
+        for _ in range(2):
+            fused(side)
             gemm(comp)
-    torch.cuda.synchronize()
-    ev = timed(side, fused_on, reps_f)
-    torch.cuda.synchronize()
-    fused_solo = [s.elapsed_time(e) for s, e in ev]
-    ev = timed(comp, gemm, 20)
-    torch.cuda.synchronize()
-    gemm_solo = [s.elapsed_time(e) for s, e in ev]
-    # concurrent: enough GEMMs to cover three times the fused calls
-    n_gemm = int(3 * reps_f * np.median(fused_solo) / np.median(gemm_solo)) + 10
-    evg = timed(comp, gemm, n_gemm)
-    evf = timed(side, fused_on, reps_f)
-    torch.cuda.synchronize()
-    gemm_conc = [s.elapsed_time(e) for s, e in evg]
-    fused_conc = [s.elapsed_time(e) for s, e in evf]
-    # GEMMs that ran while the fused calls were in flight: the middle third
-    lo, hi = n_gemm // 3, 2 * n_gemm // 3
-    med = lambda x: float(np.median(x))
-    line = {
-        "metric": "interference: slowdown of the fused call and of a bf16 GEMM when run concurrently",
-        "workload": wl.name, "gemm": "bf16 8192x8192x8192 (torch.matmul)",
-        "fused_solo_ms": round(med(fused_solo), 4),
-        "fused_concurrent_ms": round(med(fused_conc), 4),
-        "fused_slowdown": round(med(fused_conc) / med(fused_solo), 3),
-        "gemm_solo_ms": round(med(gemm_solo), 4),
-        "gemm_concurrent_ms": round(med(gemm_conc[lo:hi]), 4),
-        "gemm_slowdown": round(med(gemm_conc[lo:hi]) / med(gemm_solo), 3),
-        "gemm_solo_tflops": round(2 * 8192**3 / (med(gemm_solo) * 1e-3) / 1e12, 1),
-        "fused_reps": reps_f, "gemm_reps": n_gemm,
-        "streams": "default priority, separate streams",
-    }
-    print(json.dumps(line), flush=True)
+        torch.cuda.synchronize()
+        origin = torch.cuda.Event(enable_timing=True)
+        origin.record(torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        ev = enqueue(side, fused, args.steps)
+        torch.cuda.synchronize()
+        f_solo = spans(origin, ev)
+        ev = enqueue(comp, gemm, 30)
+        torch.cuda.synchronize()
+        g_solo = spans(origin, ev)
+        fs_ms = med([e - b for b, e in f_solo])
+        gs_ms = med([e - b for b, e in g_solo])
+        n_gemm = int(3 * args.steps * fs_ms / gs_ms) + 10
+        evg = enqueue(comp, gemm, n_gemm)
+        evf = enqueue(side, fused, args.steps)
+        torch.cuda.synchronize()
+        g_conc, f_conc = spans(origin, evg), spans(origin, evf)
+        w0, w1 = min(b for b, _ in f_conc), max(e for _, e in f_conc)
+        inside = [e - b for b, e in g_conc if b >= w0 and e <= w1]
+        busy = sum(max(0.0, min(e, w1) - max(b, w0)) for b, e in g_conc) / (w1 - w0)
+        fc_ms = med([e - b for b, e in f_conc])
+        gc_ms = med(inside)
+        line = {
+            "metric": "interference: fused aggregate+AdamW vs a concurrent bf16 GEMM loop",
+            "workload": wl.name, "gemm": "bf16 8192x8192x8192 (torch.matmul)",
+            "cu_split": None if k == 0 else {"fused_cus": k, "gemm_cus": n_cu - k},
+            "fused_solo_ms": round(fs_ms, 4), "fused_concurrent_ms": round(fc_ms, 4),
+            "fused_slowdown": round(fc_ms / fs_ms, 3),
+            "fused_solo_TBps": round(wl.n * 58 / (fs_ms * 1e-3) / 1e12, 3),
+            "gemm_solo_ms": round(gs_ms, 4),
+            "gemm_concurrent_ms": None if gc_ms is None else round(gc_ms, 4),
+            "gemm_slowdown": None if gc_ms is None else round(gc_ms / gs_ms, 3),
+            "gemm_solo_tflops": round(2 * 8192**3 / (gs_ms * 1e-3) / 1e12, 1),
+            "gemms_inside_fused_window": len(inside),
+            "gemm_busy_frac": round(busy, 3),
+            "fused_reps": args.steps,
+            "streams": "default priority" + ("" if k == 0 else ", CU-masked"),
+        }
+        print(json.dumps(line), flush=True)
+        torch.cuda.synchronize()
+        for hip, h in handles:
+            hip.hipStreamDestroy(h)
 
 
 def run_copy_probe(args):
-    """A plain device-to-device copy of COPY_PROBE_ELEMS fp32 elements
-    (torch's elementwise copy kernel): known bytes read and written per
-    launch, against which the HBM byte counters of the fused kernel are
-    scaled."""
+    """The plain copy kernel of libdisdp_probe.so over COPY_PROBE_ELEMS fp32
+    elements: known bytes read and written per launch, against which the HBM
+    byte counters of the fused kernel are scaled."""
     import numpy as np
     import torch
     torch.cuda.set_device(0)
+    L = probe_lib()
     src = torch.ones(COPY_PROBE_ELEMS, device="cuda")
     dst = torch.empty_like(src)
-    for _ in range(args.warmup):
-        dst.copy_(src)
-    torch.cuda.synchronize()
+    nbytes = COPY_PROBE_ELEMS * 4
     s = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        assert L.disdp_probe_copy(src.data_ptr(), dst.data_ptr(), nbytes, s.cuda_stream or None) == 0
+    torch.cuda.synchronize()
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(args.steps)]
     for a, b in ev:
         a.record(s)
-        dst.copy_(src)
+        assert L.disdp_probe_copy(src.data_ptr(), dst.data_ptr(), nbytes, s.cuda_stream or None) == 0
         b.record(s)
     torch.cuda.synchronize()
     ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
-    nbytes = COPY_PROBE_ELEMS * 4
-    print(json.dumps({"metric": "copy probe", "bytes_read_per_launch": nbytes,
+    assert torch.equal(src[:4096], dst[:4096]) and torch.equal(src[-4096:], dst[-4096:])
+    print(json.dumps({"metric": "copy probe", "kernel": "copy16 (libdisdp_probe.so)",
+                      "bytes_read_per_launch": nbytes,
                       "bytes_written_per_launch": nbytes, "avg_ms": round(ms, 4),
                       "GBps": round(2 * nbytes / (ms * 1e-3) / 1e9, 1),
                       "launches": args.steps}), flush=True)
@@ -359,6 +421,8 @@ def main(argv=None):
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-copy-ceiling", action="store_true")
     ap.add_argument("--interference", action="store_true")
+    ap.add_argument("--cu-split", default="0,32,64,128",
+                    help="interference: CUs given to the fused call (0 = shared)")
     ap.add_argument("--copy-probe", action="store_true")
     args = ap.parse_args(argv)
     world = int(os.environ.get("WORLD_SIZE", "1"))
