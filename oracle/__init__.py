@@ -9,7 +9,10 @@ What it computes (arXiv 2409.00918):
   * ``aggregate_f32``   -- the switch's W-way gradient sum in worker order
                           (Section III-A overall architecture; Section III-C).
   * ``aggregate_fixed`` -- the same sum in the integer format of the SmartNIC
-                          format-conversion unit (Section III-B), bit-exact.
+                          format-conversion unit (Section III-B), bit-exact;
+                          contributions may be float32, bf16 or int32 that is
+                          already in that format.
+  * ``quantize_array``  -- that format conversion over a buffer.
   * ``adamw``           -- the parameter server's mixed-precision Adam step,
                           step 5 of the backward stage (Section III-D, Table III).
   * ``fused``           -- the two composed, element by element.
@@ -32,7 +35,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "disdp_oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
 
-DT_F32, DT_BF16 = 0, 1
+DT_F32, DT_BF16, DT_I32 = 0, 1, 2
 AGG_FP32, AGG_FIXED = 0, 1
 
 # gcc flags: IEEE binary32 with no contraction and no fast-math shortcuts.
@@ -67,6 +70,8 @@ def lib() -> ctypes.CDLL:
         L.oracle_bf16_to_f32.argtypes = [ctypes.c_uint16]
         L.oracle_quantize.restype = ctypes.c_int32
         L.oracle_quantize.argtypes = [f32, ci]
+        L.oracle_quantize_array.restype = None
+        L.oracle_quantize_array.argtypes = [vp, ci, i64, ci, vp]
         L.oracle_aggregate_f32.restype = None
         L.oracle_aggregate_f32.argtypes = [vp, ci, ci, i64, vp]
         L.oracle_aggregate_fixed.restype = None
@@ -99,6 +104,8 @@ def _grad_dtype(gs: Sequence[np.ndarray]) -> int:
         return DT_F32
     if d == np.uint16:        # bf16 carried as raw bits
         return DT_BF16
+    if d == np.int32:         # contributions already in the integer format
+        return DT_I32
     raise TypeError(f"unsupported gradient dtype {d}")
 
 
@@ -135,10 +142,20 @@ def bf16_to_f32(h) -> np.ndarray:
 
 
 def quantize(x, k: int) -> np.ndarray:
+    """Element by element through oracle_quantize (float32 input)."""
     x = np.ascontiguousarray(x, dtype=np.float32).ravel()
     L = lib()
     return np.fromiter((L.oracle_quantize(float(v), k) for v in x),
                        dtype=np.int32, count=x.size)
+
+
+def quantize_array(g: np.ndarray, k: int) -> np.ndarray:
+    """oracle_quantize_array over a float32 or bf16 (uint16 bits) buffer."""
+    g = np.ascontiguousarray(g)
+    out = np.empty(g.size, dtype=np.int32)
+    lib().oracle_quantize_array(g.ctypes.data, _grad_dtype([g]), g.size, k,
+                                out.ctypes.data)
+    return out
 
 
 def scalars(lr, beta1, beta2, wd, t) -> np.ndarray:

@@ -34,7 +34,7 @@
 #include <string.h>
 
 /* ---- gradient element types ------------------------------------------- */
-enum { ORACLE_DT_F32 = 0, ORACLE_DT_BF16 = 1 };
+enum { ORACLE_DT_F32 = 0, ORACLE_DT_BF16 = 1, ORACLE_DT_I32 = 2 };
 enum { ORACLE_AGG_FP32 = 0, ORACLE_AGG_FIXED = 1 };
 
 /* bf16 -> fp32: a bf16 value is the top half of the fp32 with the same
@@ -103,6 +103,24 @@ int32_t oracle_quantize(float x, int k)
     return (int32_t)r;
 }
 
+/* The format conversion over a whole buffer, as a worker's NIC would apply
+ * it before pushing (Section III-B): out[i] = quantize(g[i], k). */
+void oracle_quantize_array(const void *g, int gdtype, int64_t n, int k,
+                           int32_t *out)
+{
+    for (int64_t i = 0; i < n; ++i)
+        out[i] = oracle_quantize(load_grad(g, gdtype, i), k);
+}
+
+/* The integer a contribution brings to the switch: float contributions are
+ * converted here; int32 contributions arrive already converted. */
+static int32_t contribution_q(const void *buf, int gdtype, int64_t i, int k)
+{
+    if (gdtype == ORACLE_DT_I32)
+        return ((const int32_t *)buf)[i];
+    return oracle_quantize(load_grad(buf, gdtype, i), k);
+}
+
 /* Integer sum over the W workers (in a 64-bit accumulator, so the sum is
  * exact and independent of the order in which contributions arrive), then
  * one saturation to int32, then the conversion back to float: int32 -> fp32
@@ -113,7 +131,7 @@ void oracle_aggregate_fixed(const void *const *g, int W, int gdtype, int64_t n,
     for (int64_t i = 0; i < n; ++i) {
         int64_t s = 0;
         for (int w = 0; w < W; ++w)
-            s += (int64_t)oracle_quantize(load_grad(g[w], gdtype, i), k);
+            s += (int64_t)contribution_q(g[w], gdtype, i, k);
         int32_t a;
         if (s > (int64_t)INT32_MAX)
             a = INT32_MAX;
@@ -212,7 +230,7 @@ void oracle_fused(const void *const *g, int W, int gdtype, int64_t n, int mode,
         for (int w = 0; w < W; ++w)
             gi[w] = (gdtype == ORACLE_DT_BF16)
                         ? (const void *)((const uint16_t *)g[w] + i)
-                        : (const void *)((const float *)g[w] + i);
+                        : (const void *)((const float *)g[w] + i);  /* f32, i32: 4 bytes */
         float a;
         if (mode == ORACLE_AGG_FIXED) {
             int32_t ai;

@@ -574,3 +574,52 @@ def test_table3_byte_and_flop_accounting():
         for g_, p_ in zip(got, (flops, mem, ssd)):
             unit = 1.0 if p_ >= 100 else 0.1      # last printed digit
             assert abs(g_ - p_) <= unit, (gbps, stage, got)
+
+
+# ----------------------------------------------------------------------------
+# the format conversion as a producer, and int32 contributions
+# ----------------------------------------------------------------------------
+@pytest.mark.parametrize("gdtype,k", [("f32", 24), ("f32", 0), ("bf16", 24), ("bf16", 30)])
+def test_quantize_array_matches_exact_rational(gdtype, k):
+    g = synth.host_grads(70, 0, 1, 4000, 1e-3, gdtype=gdtype, outlier_frac=0.02,
+                         outlier_scale=1e6)[0]
+    vals = oracle.bf16_to_f32(g) if gdtype == "bf16" else g
+    want = np.array([exact_quantize(v, k) for v in vals], dtype=np.int64)
+    assert np.array_equal(oracle.quantize_array(g, k).astype(np.int64), want)
+
+
+def test_aggregate_fixed_of_int32_contributions_is_the_exact_sum():
+    rng = np.random.default_rng(71)
+    n, W = 3000, 7
+    gs = [rng.integers(I32_MIN, I32_MAX, n, dtype=np.int64, endpoint=True).astype(np.int32)
+          for _ in range(W)]
+    gs[0][:5] = I32_MAX
+    gs[1][:5] = I32_MAX                       # overflow: clamps to INT32_MAX
+    gs[2][5:9] = I32_MIN
+    gs[3][5:9] = I32_MIN
+    small = [rng.integers(-1000, 1000, n).astype(np.int32) for _ in range(3)]
+    for case in (gs, small):
+        ai, af = oracle.aggregate_fixed(case, 24)
+        s = [sum(int(c[i]) for c in case) for i in range(n)]
+        want = np.array([max(I32_MIN, min(I32_MAX, x)) for x in s], dtype=np.int64)
+        assert np.array_equal(ai.astype(np.int64), want)
+        want_f = np.array([np.ldexp(np.float32(float(a)), -24) for a in want], np.float32)
+        assert np.array_equal(bits(af), bits(want_f))
+
+
+@pytest.mark.parametrize("gdtype", ["f32", "bf16"])
+def test_quantise_then_aggregate_equals_aggregate_of_floats(gdtype):
+    # the switch sums what the NICs produced: converting first and summing
+    # int32 contributions gives the same bits as converting inside the sum
+    n, W, k = 2500, 6, 24
+    gs = synth.host_grads(72, 0, W, n, 1e-4, gdtype=gdtype, outlier_frac=0.01,
+                          outlier_scale=1e5)
+    qs = [oracle.quantize_array(g, k) for g in gs]
+    a_i, a_f = oracle.aggregate_fixed(gs, k)
+    b_i, b_f = oracle.aggregate_fixed(qs, k)
+    assert np.array_equal(a_i, b_i) and np.array_equal(bits(a_f), bits(b_f))
+    p, m, v = synth.host_state(72, n, mv_sigma=1e-4)
+    x = oracle.fused(gs, p, m, v, mode=oracle.AGG_FIXED, frac_bits=k, t=2, **HP)
+    y = oracle.fused(qs, p, m, v, mode=oracle.AGG_FIXED, frac_bits=k, t=2, **HP)
+    for key in ("p", "m", "v", "p16"):
+        assert np.array_equal(x[key], y[key])
