@@ -176,6 +176,18 @@ def run_bench(args):
     dg, dp, dm, dv, d16 = allocate(wl)
     hp = hparams(wl)
     stream = torch.cuda.current_stream()
+    contrib = "float"
+    if args.contributions == "i32":
+        # the workers' NICs converted their gradients before the push: the
+        # fused call sums int32 contributions (fixed mode at the shard's scale)
+        if wl.mode != "fixed":
+            raise SystemExit("--contributions i32 needs a fixed-point workload")
+        for w in range(wl.W):
+            q = torch.empty(wl.n, dtype=torch.int32, device="cuda")
+            dd.quantize(dg[w], q, frac_bits=wl.frac_bits)
+            dg[w] = q
+        torch.cuda.synchronize()
+        contrib = "int32"
 
     def step(t):
         dd.aggregate_adam(dg, dp, dm, dv, d16, lr=hp["lr"], beta1=hp["beta1"],
@@ -212,7 +224,7 @@ def run_bench(args):
 
     copy_gbps = None if args.no_copy_ceiling else copy_ceiling_gbps()
 
-    gb = 2 if wl.gdtype == "bf16" else 4
+    gb = 2 if (wl.gdtype == "bf16" and contrib == "float") else 4
     bpe = dd.algorithmic_bytes_per_element(wl.W, gb)
     algo_bytes = wl.n * bpe
     achieved = algo_bytes / (avg_kernel_ms * 1e-3) / 1e9
@@ -246,7 +258,8 @@ def run_bench(args):
         "achieved_hbm_tb_s": round(achieved / 1e3, 3),
         "hbm_frac_of_peak": round(achieved / HBM_PEAK_GBPS, 4),
         "config": {"workload": wl.name, "n": wl.n, "W": wl.W,
-                   "grad_dtype": wl.gdtype, "aggregation": wl.mode,
+                   "grad_dtype": wl.gdtype if contrib == "float" else "i32",
+                   "aggregation": wl.mode,
                    "frac_bits": wl.frac_bits, "optimizer": "AdamW",
                    "lr": wl.lr, "betas": [wl.beta1, wl.beta2], "eps": wl.eps,
                    "weight_decay": wl.wd, "bf16_copy": True,
@@ -255,6 +268,45 @@ def run_bench(args):
         "cpu_baseline": base,
     }
     print(json.dumps(line), flush=True)
+
+
+def run_quantize(args):
+    """The worker-side format conversion (disdp_quantize) over each of the
+    shard's W contributions: s_g bytes read and 4 written per element."""
+    import numpy as np
+    import torch
+    import paper_2409_00918_amd as dd
+    import synth
+    wl = synth.WORKLOADS[args.workload]
+    torch.cuda.set_device(0)
+    dd.lib()
+    dg = synth.device_grads(wl.wid, 1, wl.W, wl.n, wl.sigma, gdtype=wl.gdtype,
+                            outlier_frac=wl.outlier_frac, outlier_scale=wl.outlier_scale)
+    out = torch.empty(wl.n, dtype=torch.int32, device="cuda")
+    k = wl.frac_bits or 24
+    s = torch.cuda.current_stream()
+    for w in range(min(args.warmup, wl.W)):
+        dd.quantize(dg[w], out, frac_bits=k)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    for i, (a, b) in enumerate(ev):
+        a.record(s)
+        dd.quantize(dg[i % wl.W], out, frac_bits=k)
+        b.record(s)
+    torch.cuda.synchronize()
+    ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    gb = 2 if wl.gdtype == "bf16" else 4
+    achieved = wl.n * (gb + 4) / (ms * 1e-3) / 1e9
+    print(json.dumps({"metric": "format conversion (disdp_quantize), G elements/s",
+                      "value": round(wl.n / (ms * 1e-3) / 1e9, 3), "unit": "G elements/s",
+                      "avg_kernel_ms": round(ms, 4), "steps": args.steps,
+                      "config": {"workload": wl.name, "n": wl.n, "grad_dtype": wl.gdtype,
+                                 "frac_bits": k},
+                      "roofline": {"bound": "hbm", "achieved": round(achieved, 1),
+                                   "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                                   "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                                   "algorithmic_bytes_per_element": gb + 4}}), flush=True)
 
 
 def _cu_mask_stream(first_cu: int, count: int, total: int):
@@ -424,6 +476,10 @@ def main(argv=None):
     ap.add_argument("--cu-split", default="0,32,64,128",
                     help="interference: CUs given to the fused call (0 = shared)")
     ap.add_argument("--copy-probe", action="store_true")
+    ap.add_argument("--quantize", action="store_true",
+                    help="time the format conversion over the shard's contributions")
+    ap.add_argument("--contributions", choices=["float", "i32"], default="float",
+                    help="i32: feed the fused call pre-quantised contributions")
     args = ap.parse_args(argv)
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus > 1 or world > 1:
@@ -435,6 +491,8 @@ def main(argv=None):
         run_interference(args)
     elif args.copy_probe:
         run_copy_probe(args)
+    elif args.quantize:
+        run_quantize(args)
     else:
         run_bench(args)
     return 0

@@ -14,7 +14,9 @@
  *   disdp_aggregate      -- the W-way reduction alone (the switch's job),
  *   disdp_adam_step      -- the optimizer step alone (step 5),
  *   disdp_aggregate_adam -- both in one pass over memory, with the bf16
- *                           parameter copy fused into the store.
+ *                           parameter copy fused into the store;
+ *   disdp_quantize       -- the worker-side conversion of a gradient into the
+ *                           integer format the fixed-point mode sums.
  *
  * The calls follow the shape of the paper's asynchronous push/pull API
  * (Table II: a buffer pointer and a length; completion awaited through a
@@ -71,8 +73,11 @@ typedef enum {
 
 /* Element type of the W gradient contributions.  Workers produce fp16/bf16
  * or fp32 gradients (Section III-B "Format Conversion Unit"); bf16 is
- * widened to fp32 exactly before any arithmetic. */
-typedef enum { DISDP_DT_F32 = 0, DISDP_DT_BF16 = 1 } disdp_dtype_t;
+ * widened to fp32 exactly before any arithmetic.  DISDP_DT_I32 marks
+ * contributions already converted to the switch's integer format at scale
+ * 2^frac_bits (the output of disdp_quantize); they are summed as they are,
+ * so they are accepted in DISDP_AGG_FIXED mode only. */
+typedef enum { DISDP_DT_F32 = 0, DISDP_DT_BF16 = 1, DISDP_DT_I32 = 2 } disdp_dtype_t;
 
 /* How the W contributions are summed.
  *  DISDP_AGG_FP32   acc = g_0[i]; acc = acc + g_w[i] for w = 1 .. W-1, in
@@ -110,7 +115,7 @@ typedef struct {
 /* W-way reduction of one shard (the SmartSwitch's aggregation, Section
  * III-A and III-C "Packet Transport Procedure").
  *   grads       host array of W device pointers, each to n elements of
- *               `gdtype`; 1 <= W <= 64.
+ *               `gdtype`; 1 <= W <= 64.  DISDP_DT_I32 only in fixed mode.
  *   mode        DISDP_AGG_FP32 or DISDP_AGG_FIXED; frac_bits = k in [0, 30]
  *               (checked in fixed mode only).
  *   agg_out_f32 fp32 aggregate (n elements).  Required in FP32 mode.
@@ -152,6 +157,22 @@ disdp_status_t disdp_aggregate_adam(const void *const *grads, int W,
                                     float *agg_out_f32, int32_t *agg_out_i32,
                                     const disdp_adamw_hparams_t *hp,
                                     hipStream_t stream);
+
+/* The float-to-integer format conversion a worker's NIC applies before
+ * pushing its gradient to an integer-only switch (Section III-B "Format
+ * Conversion Unit", following SwitchML): for every i,
+ *   out[i] = sat32(round_half_even(grad[i] * 2^frac_bits)),
+ * NaN -> 0, +-inf and out-of-range values saturate -- the same conversion
+ * DISDP_AGG_FIXED applies inside the aggregation, so W buffers converted here
+ * and aggregated as DISDP_DT_I32 give the same bits as aggregating the W
+ * float buffers in fixed mode.
+ *   grad        n elements of `gdtype` (DISDP_DT_F32 or DISDP_DT_BF16).
+ *   frac_bits   k in [0, 30].
+ *   out         n int32 (device), must not overlap grad.
+ * Errors as for the other calls (DISDP_ERR_UNSUPPORTED for DISDP_DT_I32
+ * input). */
+disdp_status_t disdp_quantize(const void *grad, disdp_dtype_t gdtype, int64_t n,
+                              int frac_bits, int32_t *out, hipStream_t stream);
 
 /* A static, NUL-terminated English name for a status code (never NULL;
  * unknown codes give "unknown status"). */

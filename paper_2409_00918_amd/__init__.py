@@ -13,6 +13,7 @@ call raises.
 ``aggregate``       -- the reduction alone            (disdp_aggregate)
 ``adam_step``       -- the optimizer step alone       (disdp_adam_step)
 ``aggregate_adam``  -- both in one pass               (disdp_aggregate_adam)
+``quantize``        -- a worker's float -> int32 conversion (disdp_quantize)
 """
 from __future__ import annotations
 
@@ -25,12 +26,12 @@ LIB_PATH = os.path.join(_PKG, "libdisdp.so")
 
 # Status codes, dtypes and modes (values fixed by include/disdp.h).
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_ALIAS, ERR_HIP = 0, 1, 2, 3, 4
-DT_F32, DT_BF16 = 0, 1
+DT_F32, DT_BF16, DT_I32 = 0, 1, 2
 AGG_FP32, AGG_FIXED = 0, 1
 MAX_W = 64
 
 EXPORTS = ("disdp_aggregate", "disdp_adam_step", "disdp_aggregate_adam",
-           "disdp_status_string")
+           "disdp_quantize", "disdp_status_string")
 
 
 class AdamWHParams(ctypes.Structure):
@@ -89,6 +90,8 @@ def lib() -> ctypes.CDLL:
         L.disdp_aggregate_adam.argtypes = [vp, ci, ci, i64, ci, ci, vp, vp, vp,
                                            vp, vp, vp,
                                            ctypes.POINTER(AdamWHParams), vp]
+        L.disdp_quantize.restype = ci
+        L.disdp_quantize.argtypes = [vp, ci, i64, ci, vp, vp]
         L.disdp_status_string.restype = ctypes.c_char_p
         L.disdp_status_string.argtypes = [ci]
         _lib = L
@@ -112,6 +115,11 @@ def raw_aggregate(grad_ptrs, W, gdtype, n, mode, frac_bits, agg_f32, agg_i32,
     return lib().disdp_aggregate(arr, W, gdtype, n, mode, frac_bits,
                                  agg_f32 or None, agg_i32 or None,
                                  stream or None)
+
+
+def raw_quantize(grad, gdtype, n, frac_bits, out, stream) -> int:
+    return lib().disdp_quantize(grad or None, gdtype, n, frac_bits, out or None,
+                                stream or None)
 
 
 def raw_adam_step(grad, param, m, v, p16, n, hp: Optional[AdamWHParams],
@@ -152,6 +160,8 @@ def _grad_dtype(t) -> int:
         return DT_F32
     if t.dtype in (torch.bfloat16, torch.int16, torch.uint16):
         return DT_BF16
+    if t.dtype == torch.int32:
+        return DT_I32
     raise TypeError(f"unsupported gradient dtype {t.dtype}")
 
 
@@ -193,8 +203,8 @@ def _grads(grads):
         raise ValueError("at least one contribution is needed")
     n = grads[0].numel()
     gdt = _grad_dtype(grads[0])
-    allowed = (torch.float32,) if gdt == DT_F32 else \
-        (torch.bfloat16, torch.int16, torch.uint16)
+    allowed = {DT_F32: (torch.float32,), DT_I32: (torch.int32,)}.get(
+        gdt, (torch.bfloat16, torch.int16, torch.uint16))
     ptrs = [_dev_ptr(g, f"grads[{i}]", n, allowed) for i, g in enumerate(grads)]
     return grads, ptrs, gdt, n
 
@@ -247,6 +257,21 @@ def aggregate_adam(grads, param, m, v, param_bf16_out=None, *, lr, beta1,
         _hparams(lr, beta1, beta2, eps, weight_decay, step, grad_scale),
         _stream(stream, grads[0]))
     _check(st, "disdp_aggregate_adam")
+
+
+def quantize(grad, out, *, frac_bits: int, stream=None) -> None:
+    """out (int32) = the switch's integer format of `grad` (float32 or bf16)
+    at scale 2^frac_bits, saturating."""
+    torch = _torch()
+    n = grad.numel()
+    gdt = _grad_dtype(grad)
+    if gdt == DT_I32:
+        raise TypeError("quantize takes float32 or bf16 input")
+    allowed = (torch.float32,) if gdt == DT_F32 else \
+        (torch.bfloat16, torch.int16, torch.uint16)
+    st = raw_quantize(_dev_ptr(grad, "grad", n, allowed), gdt, n, frac_bits,
+                      _dev_ptr(out, "out", n, (torch.int32,)), _stream(stream, grad))
+    _check(st, "disdp_quantize")
 
 
 def algorithmic_bytes_per_element(W: int, grad_bytes: int, adam: bool = True,

@@ -28,6 +28,9 @@ bool overlaps(Span a, Span b) { return a.lo < b.hi && b.lo < a.hi; }
 
 int grad_bytes(int gdtype) { return gdtype == DISDP_DT_BF16 ? 2 : 4; }
 
+// Alignment the vector kernels need for a contribution buffer: 4 elements.
+uintptr_t grad_vector_align(int gdtype) { return gdtype == DISDP_DT_BF16 ? 8 : 16; }
+
 // Largest n accepted: keeps every byte count far below 2^63.
 constexpr int64_t kMaxN = int64_t(1) << 56;
 
@@ -35,10 +38,12 @@ disdp_status_t check_counts(int W, int gdtype, int64_t n, int mode, int frac_bit
 {
     if (n < 0 || n > kMaxN || W < 1 || W > disdp::kMaxW)
         return DISDP_ERR_INVALID_ARG;
-    if (gdtype != DISDP_DT_F32 && gdtype != DISDP_DT_BF16)
+    if (gdtype != DISDP_DT_F32 && gdtype != DISDP_DT_BF16 && gdtype != DISDP_DT_I32)
         return DISDP_ERR_UNSUPPORTED;
     if (mode != DISDP_AGG_FP32 && mode != DISDP_AGG_FIXED)
         return DISDP_ERR_UNSUPPORTED;
+    if (gdtype == DISDP_DT_I32 && mode != DISDP_AGG_FIXED)
+        return DISDP_ERR_UNSUPPORTED;  // integer contributions are summed as integers
     if (mode == DISDP_AGG_FIXED && (frac_bits < 0 || frac_bits > 30))
         return DISDP_ERR_INVALID_ARG;
     return DISDP_OK;
@@ -161,7 +166,7 @@ disdp_status_t run(const void *const *grads, int W, int gdtype, int64_t n,
     // 8-byte bf16 groups.
     bool vec = true;
     for (int w = 0; w < W; ++w)
-        vec = vec && aligned(grads[w], gdtype == DISDP_DT_BF16 ? 8 : 16);
+        vec = vec && aligned(grads[w], grad_vector_align(gdtype));
     for (const void *p : {static_cast<const void *>(param), static_cast<const void *>(m),
                           static_cast<const void *>(v), static_cast<const void *>(agg_f32),
                           static_cast<const void *>(agg_i32)})
@@ -209,6 +214,31 @@ disdp_status_t disdp_aggregate_adam(const void *const *grads, int W,
     return run(grads, W, gdtype, n, mode, frac_bits, param, m, v, param_bf16_out,
                agg_out_f32, agg_out_i32, hp, /*adam=*/true,
                /*agg_f32_required=*/false, stream);
+}
+
+disdp_status_t disdp_quantize(const void *grad, disdp_dtype_t gdtype, int64_t n,
+                              int frac_bits, int32_t *out, hipStream_t stream)
+{
+    if (n < 0 || n > kMaxN)
+        return DISDP_ERR_INVALID_ARG;
+    if (gdtype != DISDP_DT_F32 && gdtype != DISDP_DT_BF16)
+        return DISDP_ERR_UNSUPPORTED;
+    if (frac_bits < 0 || frac_bits > 30)
+        return DISDP_ERR_INVALID_ARG;
+    if (n == 0)
+        return DISDP_OK;
+    if (!grad || !out)
+        return DISDP_ERR_INVALID_ARG;
+    if (overlaps(span_of(out, n, 4), span_of(grad, n, grad_bytes(gdtype))))
+        return DISDP_ERR_ALIAS;
+    disdp::QuantizeArgs q;
+    q.g = grad;
+    q.out = out;
+    q.n = n;
+    q.gdtype = gdtype;
+    q.qscale = std::ldexp(1.0f, frac_bits);
+    const bool vec = aligned(grad, grad_vector_align(gdtype)) && aligned(out, 16);
+    return disdp::launch_quantize(q, vec, stream) == hipSuccess ? DISDP_OK : DISDP_ERR_HIP;
 }
 
 const char *disdp_status_string(disdp_status_t status)

@@ -172,11 +172,29 @@ __device__ __forceinline__ void adamw(const StepScalars &s, float agg, float &p,
 
 // ---- loading contributions -----------------------------------------------
 
+// What one element of a contribution holds once loaded: a float (fp32 or
+// widened bf16), or an int32 already in the switch's integer format.
+template <int GT>
+struct Contrib {
+    using type = float;
+};
+template <>
+struct Contrib<kGradI32> {
+    using type = int32_t;
+};
+
 // Four consecutive elements of contribution `base` at group index `grp`.
 template <int GT>
-__device__ __forceinline__ void load_group(const void *base, int64_t grp, float (&x)[4])
+__device__ __forceinline__ void load_group(const void *base, int64_t grp,
+                                           typename Contrib<GT>::type (&x)[4])
 {
-    if constexpr (GT == kGradF32) {
+    if constexpr (GT == kGradI32) {
+        const i32x4 v = ld_nt(reinterpret_cast<const i32x4 *>(base) + grp);
+        x[0] = v.x;
+        x[1] = v.y;
+        x[2] = v.z;
+        x[3] = v.w;
+    } else if constexpr (GT == kGradF32) {
         const f32x4 v = ld_nt(reinterpret_cast<const f32x4 *>(base) + grp);
         x[0] = v.x;
         x[1] = v.y;
@@ -192,9 +210,11 @@ __device__ __forceinline__ void load_group(const void *base, int64_t grp, float 
 }
 
 template <int GT>
-__device__ __forceinline__ float load_one(const void *base, int64_t i)
+__device__ __forceinline__ typename Contrib<GT>::type load_one(const void *base, int64_t i)
 {
-    if constexpr (GT == kGradF32)
+    if constexpr (GT == kGradI32)
+        return reinterpret_cast<const int32_t *>(base)[i];
+    else if constexpr (GT == kGradF32)
         return reinterpret_cast<const float *>(base)[i];
     else
         return widen_lo(reinterpret_cast<const uint16_t *>(base)[i]);
@@ -220,6 +240,17 @@ struct Acc {
             f = f + x;
         else
             s += quantize(x, qscale);
+    }
+    // contributions already in the integer format (fixed mode only)
+    __device__ __forceinline__ void first(int32_t q, float)
+    {
+        static_assert(MODE == kAggFixed, "int32 contributions are summed as integers");
+        s = q;
+    }
+    __device__ __forceinline__ void next(int32_t q, float)
+    {
+        static_assert(MODE == kAggFixed, "int32 contributions are summed as integers");
+        s += q;
     }
     // (fp32 aggregate, int32 aggregate)
     __device__ __forceinline__ float result(float dqscale, int32_t &ai) const
@@ -270,7 +301,7 @@ __device__ __forceinline__ void finish_group(const LaunchArgs &a, int64_t grp, c
 template <int W, int GT, int MODE, bool ADAM, int U>
 __device__ __forceinline__ void process_groups(const LaunchArgs &a, int64_t g0, int stride)
 {
-    float c[U][W][4];
+    typename Contrib<GT>::type c[U][W][4];
     f32x4 P[U], M[U], V[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -316,7 +347,7 @@ __device__ __forceinline__ void process_group_rt(const LaunchArgs &a, int64_t gr
     }
     Acc<MODE> acc[4];
     for (int w0 = 0; w0 < a.W; w0 += kChunk) {
-        float c[kChunk][4];
+        typename Contrib<GT>::type c[kChunk][4];
 #pragma unroll
         for (int j = 0; j < kChunk; ++j)
             if (w0 + j < a.W)
@@ -437,6 +468,37 @@ __global__ DISDP_LAUNCH_BOUNDS void element_kernel(LaunchArgs a)
         process_element<GT, MODE, ADAM>(a, i);
 }
 
+// ---- the format conversion as a producer ------------------------------------
+
+// out = quantize(g) over 4-element groups (one group per lane, one
+// 256-lane tile per block), the last n % 4 elements by block 0.
+template <int GT>
+__global__ DISDP_LAUNCH_BOUNDS void quantize_vector_kernel(QuantizeArgs q)
+{
+    const int64_t n_groups = q.n >> 2;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+    for (int64_t grp = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; grp < n_groups;
+         grp += stride) {
+        float x[4];
+        load_group<GT>(q.g, grp, x);
+        st_nt(reinterpret_cast<i32x4 *>(q.out) + grp,
+              i32x4{quantize(x[0], q.qscale), quantize(x[1], q.qscale),
+                    quantize(x[2], q.qscale), quantize(x[3], q.qscale)});
+    }
+    if (blockIdx.x == 0 && threadIdx.x < (q.n & 3)) {
+        const int64_t i = (n_groups << 2) + threadIdx.x;
+        q.out[i] = quantize(load_one<GT>(q.g, i), q.qscale);
+    }
+}
+
+template <int GT>
+__global__ DISDP_LAUNCH_BOUNDS void quantize_element_kernel(QuantizeArgs q)
+{
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < q.n; i += stride)
+        q.out[i] = quantize(load_one<GT>(q.g, i), q.qscale);
+}
+
 // ---- host side: grid sizing and dispatch --------------------------------------
 
 constexpr int kU = DISDP_UNROLL;
@@ -546,6 +608,8 @@ hipError_t dispatch_w(const LaunchArgs &a, bool vec, hipStream_t stream)
 template <bool ADAM>
 hipError_t dispatch(const LaunchArgs &a, bool vec, hipStream_t stream)
 {
+    if (a.gdtype == kGradI32)  // the front end admits int32 only in fixed mode
+        return dispatch_w<kGradI32, kAggFixed, ADAM>(a, vec, stream);
     if (a.gdtype == kGradF32)
         return a.mode == kAggFP32 ? dispatch_w<kGradF32, kAggFP32, ADAM>(a, vec, stream)
                                   : dispatch_w<kGradF32, kAggFixed, ADAM>(a, vec, stream);
@@ -559,6 +623,27 @@ hipError_t launch(const LaunchArgs &a, Kind kind, bool vector_path, hipStream_t 
 {
     return kind == kAggregateAdam ? dispatch<true>(a, vector_path, stream)
                                   : dispatch<false>(a, vector_path, stream);
+}
+
+hipError_t launch_quantize(const QuantizeArgs &q, bool vector_path, hipStream_t stream)
+{
+    const void *fn;
+    int64_t blocks;
+    if (vector_path) {
+        fn = q.gdtype == kGradBF16 ? reinterpret_cast<const void *>(&quantize_vector_kernel<kGradBF16>)
+                                   : reinterpret_cast<const void *>(&quantize_vector_kernel<kGradF32>);
+        blocks = ceil_div(q.n >> 2, kBlock);
+    } else {
+        fn = q.gdtype == kGradBF16 ? reinterpret_cast<const void *>(&quantize_element_kernel<kGradBF16>)
+                                   : reinterpret_cast<const void *>(&quantize_element_kernel<kGradF32>);
+        blocks = ceil_div(q.n, kBlock);
+    }
+    if (blocks > 0x7fffffff)
+        blocks = 0x7fffffff;   // the kernels are grid-stride
+    if (blocks < 1)
+        blocks = 1;
+    void *args[] = {const_cast<QuantizeArgs *>(&q)};
+    return hipLaunchKernel(fn, dim3(static_cast<unsigned>(blocks)), dim3(kBlock), args, 0, stream);
 }
 
 }  // namespace disdp

@@ -9,7 +9,7 @@ namespace disdp {
 
 constexpr int kMaxW = 64;
 
-enum GradType { kGradF32 = 0, kGradBF16 = 1 };
+enum GradType { kGradF32 = 0, kGradBF16 = 1, kGradI32 = 2 };
 enum AggMode { kAggFP32 = 0, kAggFixed = 1 };
 enum Kind { kAggregateOnly = 0, kAggregateAdam = 1 };
 
@@ -39,5 +39,15 @@ struct LaunchArgs {
 // 4-elements-per-lane kernels (all pointers suitably aligned).
 hipError_t launch(const LaunchArgs &a, Kind kind, bool vector_path,
                   hipStream_t stream);
+
+// The float-to-int32 format conversion of one buffer.
+struct QuantizeArgs {
+    const void *g;     // n elements of gdtype (kGradF32 or kGradBF16)
+    int32_t *out;      // n int32
+    int64_t n;
+    int gdtype;
+    float qscale;      // 2^k
+};
+hipError_t launch_quantize(const QuantizeArgs &q, bool vector_path, hipStream_t stream);
 
 }  // namespace disdp

@@ -260,3 +260,25 @@ def test_library_binds_to_the_same_hip_runtime_as_torch():
     out = subprocess.run([__import__("sys").executable, "-c", code], cwd=ROOT,
                          capture_output=True, text=True, check=True).stdout
     assert out.strip().splitlines()[-1] == "1"
+
+
+# ---------------------------------------------------------------- quantize --
+def test_quantize_argument_checks():
+    q = lambda g=A[0], dt=dd.DT_F32, n=N, k=24, out=A[1]: dd.raw_quantize(g, dt, n, k, out, 0)
+    assert q(n=-1) == dd.ERR_INVALID_ARG
+    assert q(dt=dd.DT_I32) == dd.ERR_UNSUPPORTED
+    assert q(dt=7) == dd.ERR_UNSUPPORTED
+    assert q(k=31) == dd.ERR_INVALID_ARG and q(k=-1) == dd.ERR_INVALID_ARG
+    assert q(g=0) == dd.ERR_INVALID_ARG and q(out=0) == dd.ERR_INVALID_ARG
+    assert q(g=0, out=0, n=0) == dd.OK
+    assert q(out=A[0]) == dd.ERR_ALIAS
+    assert q(out=A[0] + 4 * (N - 1)) == dd.ERR_ALIAS
+    assert q(dt=dd.DT_BF16, out=A[0] + 2 * N - 2) == dd.ERR_ALIAS
+
+
+def test_int32_contributions_only_in_fixed_mode():
+    assert agg(gdtype=dd.DT_I32, mode=dd.AGG_FP32) == dd.ERR_UNSUPPORTED
+    assert fused(gdtype=dd.DT_I32, mode=dd.AGG_FP32) == dd.ERR_UNSUPPORTED
+    # in fixed mode the combination passes the enumeration checks (and then
+    # fails here only on the planted aliasing, so nothing launches)
+    assert agg(gdtype=dd.DT_I32, mode=dd.AGG_FIXED, f32=A[2]) == dd.ERR_ALIAS

@@ -347,3 +347,65 @@ def test_tiny_shard_ten_steps_against_oracle():
         got = {"p": to_host(dp), "m": to_host(dm), "v": to_host(dv), "p16": to_host(d16)}
         assert_parity(got, want, f"step {t}")
         p, m, v = want["p"], want["m"], want["v"]
+
+
+# ------------------------------------- format conversion and int32 contributions --
+@pytest.mark.parametrize("gdtype", ["f32", "bf16"])
+@pytest.mark.parametrize("k", [0, 16, 24, 30])
+def test_quantize_matches_oracle(gdtype, k):
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    for i, n in enumerate((1, 3, 4, 5, 1023, 1025, 65541, 300_007)):
+        g = synth.host_grads(400 + k, i, 1, n, 1e-3, gdtype=gdtype, outlier_frac=0.02,
+                             outlier_scale=1e6)[0]
+        if gdtype == "f32" and n > 8:
+            g[:6] = np.array([np.inf, -np.inf, np.nan, 3e38, -3e38, 1e-45], np.float32)
+        for off in ((0, 0), (1, 3)) if n > 4 else ((0, 0),):
+            out = to_dev(np.zeros(n, np.int32), off[1])
+            dd.quantize(to_dev(g, off[0]), out, frac_bits=k)
+            t_.cuda.synchronize()
+            assert np.array_equal(to_host(out), oracle.quantize_array(g, k)), (n, off)
+
+
+@pytest.mark.parametrize("W", [1, 3, 8, 16, 20])
+def test_int32_contributions_match_oracle_and_float_path(W):
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    k = 24
+    for i, n in enumerate((2, 1027, 100_003)):
+        gs = synth.host_grads(410 + W, i, W, n, 1e-4, outlier_frac=0.01, outlier_scale=1e5)
+        qs = [oracle.quantize_array(g, k) for g in gs]
+        p, m, v = synth.host_state(410 + W, n, mv_sigma=1e-4)
+        want = oracle.fused(qs, p, m, v, mode=oracle.AGG_FIXED, frac_bits=k, t=3,
+                            want_agg_f32=True, want_agg_i32=True, **HP)
+        outs = {}
+        for label, srcs in (("int32", qs), ("float", gs)):
+            dg = [to_dev(x) for x in srcs]
+            st = [to_dev(x) for x in (p, m, v)] + [to_dev(np.zeros(n, np.uint16))]
+            dai = to_dev(np.zeros(n, np.int32))
+            daf = to_dev(np.zeros(n, np.float32))
+            dd.aggregate_adam(dg, *st, lr=HP["lr"], beta1=HP["beta1"], beta2=HP["beta2"],
+                              eps=HP["eps"], weight_decay=HP["wd"], step=3, mode="fixed",
+                              frac_bits=k, agg_out_f32=daf, agg_out_i32=dai)
+            t_.cuda.synchronize()
+            outs[label] = {"p": to_host(st[0]), "m": to_host(st[1]), "v": to_host(st[2]),
+                           "p16": to_host(st[3]), "agg_i32": to_host(dai),
+                           "agg_f32": to_host(daf)}
+        assert_parity(outs["int32"], want, f"int32 W={W} n={n}")
+        for key in outs["int32"]:
+            assert np.array_equal(outs["int32"][key], outs["float"][key]), key
+        # the aggregation alone, unaligned int32 contributions
+        dg = [to_dev(q, 1) for q in qs]
+        dai = to_dev(np.zeros(n, np.int32))
+        dd.aggregate(dg, mode="fixed", frac_bits=k, agg_out_i32=dai)
+        t_.cuda.synchronize()
+        assert np.array_equal(to_host(dai), want["agg_i32"])
+
+
+def test_int32_contributions_rejected_in_fp32_mode():
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    g = t_.zeros(8, dtype=t_.int32, device="cuda")
+    with pytest.raises(dd.DisdpError) as ei:
+        dd.aggregate([g, g], mode="fp32", agg_out_f32=t_.zeros(8, device="cuda"))
+    assert ei.value.status == dd.ERR_UNSUPPORTED
