@@ -26,9 +26,15 @@
  * ------------------
  * Ownership   The caller owns every buffer.  The library allocates nothing,
  *             keeps no state between calls, never synchronises and is
- *             re-entrant.  Array pointers are DEVICE pointers (memory the
- *             GPU can read and write); `grads` itself is a HOST array of W
- *             device pointers and is read before the call returns.
+ *             re-entrant.  `grads` is a HOST array of W pointers, read before
+ *             the call returns.
+ * Memory      Every array pointer must be one the GPU can dereference at that
+ *             address: device (or managed) memory, or pinned host memory
+ *             mapped for the device (hipHostMalloc), whose device address is
+ *             its host address.  Host-resident arrays are streamed by the
+ *             kernels over the host link -- e.g. the 12-byte states of a
+ *             shard too large for HBM, kept in host DRAM as the paper's
+ *             parameter server keeps them (Section III-D, steps 4 and 6).
  * Layout      Every array is flat and contiguous with N elements; index i
  *             is the same parameter in every array.  fp32 arrays hold IEEE
  *             binary32; bf16 arrays hold raw bf16 bit patterns (uint16_t);
@@ -39,9 +45,11 @@
  * Alignment   Any alignment is accepted.  When every pointer is 16-byte
  *             aligned (8-byte for bf16 arrays) the vector kernels run,
  *             otherwise element-wise ones; results are identical.
- * Errors      Arguments are checked on the host before any HIP call, in
- *             this order: counts and enumerations, hyperparameters, then
- *             (only when n > 0) NULL pointers, then overlap.  A failed check
+ * Errors      Arguments are checked on the host in this order: counts and
+ *             enumerations, hyperparameters, then (only when n > 0) NULL
+ *             pointers, overlap, and -- the first HIP call -- that every
+ *             array is GPU-addressable (hipPointerGetAttributes; pageable or
+ *             unknown memory gives DISDP_ERR_INVALID_ARG).  A failed check
  *             returns its code and enqueues nothing.  n == 0 returns
  *             DISDP_OK with no launch (NULL pointers are then allowed).
  *             Outputs must not overlap one another nor any input; p, m and

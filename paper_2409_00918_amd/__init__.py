@@ -166,10 +166,12 @@ def _grad_dtype(t) -> int:
 
 
 def _dev_ptr(t, name: str, n: int, dtypes) -> int:
+    """Pointer of a device tensor, or of a pinned host tensor (which the
+    library streams over the host link; it checks the mapping itself)."""
     if t is None:
         return 0
-    if not t.is_cuda:
-        raise ValueError(f"{name} must be a device tensor")
+    if not (t.is_cuda or t.is_pinned()):
+        raise ValueError(f"{name} must be a device tensor or pinned host memory")
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
     if t.numel() != n:
@@ -180,9 +182,12 @@ def _dev_ptr(t, name: str, n: int, dtypes) -> int:
 
 
 def _stream(stream, ref) -> int:
+    """The HIP stream to launch on: the one given, else torch's current
+    stream of `ref`'s device (of the current device for host tensors)."""
     torch = _torch()
     if stream is None:
-        return torch.cuda.current_stream(ref.device).cuda_stream
+        dev = ref.device if ref.is_cuda else None
+        return torch.cuda.current_stream(dev).cuda_stream
     return getattr(stream, "cuda_stream", stream)
 
 

@@ -89,6 +89,29 @@ bool aligned(const void *p, uintptr_t a)
     return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0;
 }
 
+// True when the GPU can dereference `p` at that very address: device or
+// managed memory, or pinned host memory mapped for the device at the same
+// address (hipHostMalloc).  Pageable host memory and unknown addresses are
+// refused here, so they never reach a kernel.
+bool gpu_addressable(const void *p)
+{
+    hipPointerAttribute_t at;
+    if (hipPointerGetAttributes(&at, p) != hipSuccess) {
+        (void)hipGetLastError();  // clear the error this query just recorded
+        return false;
+    }
+    switch (at.type) {
+    case hipMemoryTypeDevice:
+    case hipMemoryTypeManaged:
+    case hipMemoryTypeUnified:
+        return true;
+    case hipMemoryTypeHost:
+        return at.devicePointer == p;
+    default:
+        return false;
+    }
+}
+
 // Shared body of the three entry points.  `adam` selects the optimizer;
 // for disdp_adam_step the single contribution is the fp32 aggregate itself
 // (an aggregate of one fp32 contribution is that contribution, unrounded).
@@ -141,6 +164,16 @@ disdp_status_t run(const void *const *grads, int W, int gdtype, int64_t n,
             if (overlaps(outs[i], span_of(grads[w], n, gb)))
                 return DISDP_ERR_ALIAS;
     }
+
+    // Every array must be addressable by the GPU as given (first HIP call).
+    for (int w = 0; w < W; ++w)
+        if (!gpu_addressable(grads[w]))
+            return DISDP_ERR_INVALID_ARG;
+    for (const void *p : {static_cast<const void *>(param), static_cast<const void *>(m),
+                          static_cast<const void *>(v), static_cast<const void *>(p16),
+                          static_cast<const void *>(agg_f32), static_cast<const void *>(agg_i32)})
+        if (p && !gpu_addressable(p))
+            return DISDP_ERR_INVALID_ARG;
 
     LaunchArgs a;
     std::memset(&a, 0, sizeof a);
@@ -231,6 +264,8 @@ disdp_status_t disdp_quantize(const void *grad, disdp_dtype_t gdtype, int64_t n,
         return DISDP_ERR_INVALID_ARG;
     if (overlaps(span_of(out, n, 4), span_of(grad, n, grad_bytes(gdtype))))
         return DISDP_ERR_ALIAS;
+    if (!gpu_addressable(grad) || !gpu_addressable(out))
+        return DISDP_ERR_INVALID_ARG;
     disdp::QuantizeArgs q;
     q.g = grad;
     q.out = out;

@@ -409,3 +409,64 @@ def test_int32_contributions_rejected_in_fp32_mode():
     with pytest.raises(dd.DisdpError) as ei:
         dd.aggregate([g, g], mode="fp32", agg_out_f32=t_.zeros(8, device="cuda"))
     assert ei.value.status == dd.ERR_UNSUPPORTED
+
+
+# --------------------------------------------- host-resident (out-of-core) state --
+def _pinned(a: np.ndarray):
+    t_ = torch()
+    if a.dtype == np.uint16:
+        a = a.view(np.int16)
+    out = t_.empty(a.size, dtype=t_.from_numpy(a[:1].copy()).dtype, pin_memory=True)
+    out.copy_(t_.from_numpy(a))
+    return out
+
+
+@pytest.mark.parametrize("where", ["state", "state+contributions"])
+def test_fused_with_state_in_pinned_host_memory(where):
+    """p, m, v and the bf16 copy in pinned host DRAM (streamed by the kernel
+    over the host link), contributions in HBM or also in host memory."""
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    for mode in ("fp32", "fixed"):
+        for n in (5, 4099, 250_001):
+            gs = synth.host_grads(500, 1, 8, n, 1e-4, outlier_frac=0.01, outlier_scale=100.0)
+            p, m, v = synth.host_state(500, n, mv_sigma=1e-4)
+            dg = [(_pinned(g) if where != "state" else to_dev(g)) for g in gs]
+            hp_, hm, hv = _pinned(p), _pinned(m), _pinned(v)
+            h16 = _pinned(np.zeros(n, np.uint16))
+            dd.aggregate_adam(dg, hp_, hm, hv, h16, lr=HP["lr"], beta1=HP["beta1"],
+                              beta2=HP["beta2"], eps=HP["eps"], weight_decay=HP["wd"],
+                              step=2, mode=mode, frac_bits=24)
+            t_.cuda.synchronize()
+            want = oracle.fused(gs, p, m, v, t=2, mode=oracle.AGG_FIXED if mode == "fixed"
+                                else oracle.AGG_FP32, frac_bits=24, **HP)
+            got = {"p": hp_.numpy(), "m": hm.numpy(), "v": hv.numpy(),
+                   "p16": h16.numpy().view(np.uint16)}
+            assert_parity(got, want, f"{where} {mode} n={n}")
+
+
+def test_pageable_host_memory_is_refused_before_any_launch():
+    import ctypes
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    n = 1024
+    dev = [t_.zeros(n, device="cuda") for _ in range(2)]
+    pageable = np.zeros(n, np.float32)          # malloc'd by numpy: not mapped
+    # first confirm with the runtime itself that the buffer is unregistered,
+    # so the library call below can only be refused, never launched
+    hip = ctypes.CDLL("libamdhip64.so.7")
+
+    class Attr(ctypes.Structure):
+        _fields_ = [("type", ctypes.c_int), ("device", ctypes.c_int),
+                    ("devicePointer", ctypes.c_void_p), ("hostPointer", ctypes.c_void_p),
+                    ("isManaged", ctypes.c_int), ("allocationFlags", ctypes.c_uint)]
+    at = Attr()
+    rc = hip.hipPointerGetAttributes(ctypes.byref(at), ctypes.c_void_p(pageable.ctypes.data))
+    hip.hipGetLastError()
+    if not (rc != 0 or at.type == 0):
+        pytest.skip(f"runtime reports the pageable buffer as registered (rc={rc}, type={at.type})")
+    st = dd.raw_aggregate([dev[0].data_ptr(), dev[1].data_ptr()], 2, dd.DT_F32, n,
+                          dd.AGG_FP32, 0, pageable.ctypes.data, 0, 0)
+    assert st == dd.ERR_INVALID_ARG
+    st = dd.raw_quantize(pageable.ctypes.data, dd.DT_F32, n, 24, dev[0].data_ptr(), 0)
+    assert st == dd.ERR_INVALID_ARG
