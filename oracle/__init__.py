@@ -24,6 +24,7 @@ operation order documented there.  Every function is pinned by
 """
 from __future__ import annotations
 
+import contextlib
 import ctypes
 import os
 import subprocess
@@ -55,39 +56,70 @@ def build(force: bool = True) -> str:
 _lib = None
 
 
+def load_library(path: str) -> ctypes.CDLL:
+    """Load an oracle build from `path` and declare its signatures."""
+    L = ctypes.CDLL(path)
+    vp, i64, f32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_float
+    ci = ctypes.c_int
+    L.oracle_bf16_rne.restype = ctypes.c_uint16
+    L.oracle_bf16_rne.argtypes = [f32]
+    L.oracle_bf16_to_f32.restype = f32
+    L.oracle_bf16_to_f32.argtypes = [ctypes.c_uint16]
+    L.oracle_quantize.restype = ctypes.c_int32
+    L.oracle_quantize.argtypes = [f32, ci]
+    L.oracle_quantize_array.restype = None
+    L.oracle_quantize_array.argtypes = [vp, ci, i64, ci, vp]
+    L.oracle_aggregate_f32.restype = None
+    L.oracle_aggregate_f32.argtypes = [vp, ci, ci, i64, vp]
+    L.oracle_aggregate_fixed.restype = None
+    L.oracle_aggregate_fixed.argtypes = [vp, ci, ci, i64, ci, vp, vp]
+    L.oracle_scalars.restype = None
+    L.oracle_scalars.argtypes = [f32, f32, f32, f32, i64, vp]
+    L.oracle_adamw.restype = None
+    L.oracle_adamw.argtypes = [vp, vp, vp, vp, vp, i64,
+                               f32, f32, f32, f32, f32, i64, f32]
+    L.oracle_fused.restype = None
+    L.oracle_fused.argtypes = [vp, ci, ci, i64, ci, ci, vp, vp, vp, vp,
+                               vp, vp, f32, f32, f32, f32, f32, i64, f32]
+    L.oracle_mxcsr_ftz_daz.restype = ctypes.c_uint
+    L.oracle_mxcsr_ftz_daz.argtypes = []
+    return L
+
+
 def lib() -> ctypes.CDLL:
     """The loaded oracle library (built on first use if it is missing)."""
     global _lib
     if _lib is None:
         if not os.path.exists(_LIB):
             build()
-        L = ctypes.CDLL(_LIB)
-        vp, i64, f32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_float
-        ci = ctypes.c_int
-        L.oracle_bf16_rne.restype = ctypes.c_uint16
-        L.oracle_bf16_rne.argtypes = [f32]
-        L.oracle_bf16_to_f32.restype = f32
-        L.oracle_bf16_to_f32.argtypes = [ctypes.c_uint16]
-        L.oracle_quantize.restype = ctypes.c_int32
-        L.oracle_quantize.argtypes = [f32, ci]
-        L.oracle_quantize_array.restype = None
-        L.oracle_quantize_array.argtypes = [vp, ci, i64, ci, vp]
-        L.oracle_aggregate_f32.restype = None
-        L.oracle_aggregate_f32.argtypes = [vp, ci, ci, i64, vp]
-        L.oracle_aggregate_fixed.restype = None
-        L.oracle_aggregate_fixed.argtypes = [vp, ci, ci, i64, ci, vp, vp]
-        L.oracle_scalars.restype = None
-        L.oracle_scalars.argtypes = [f32, f32, f32, f32, i64, vp]
-        L.oracle_adamw.restype = None
-        L.oracle_adamw.argtypes = [vp, vp, vp, vp, vp, i64,
-                                   f32, f32, f32, f32, f32, i64, f32]
-        L.oracle_fused.restype = None
-        L.oracle_fused.argtypes = [vp, ci, ci, i64, ci, ci, vp, vp, vp, vp,
-                                   vp, vp, f32, f32, f32, f32, f32, i64, f32]
-        L.oracle_mxcsr_ftz_daz.restype = ctypes.c_uint
-        L.oracle_mxcsr_ftz_daz.argtypes = []
-        _lib = L
+        _lib = load_library(_LIB)
     return _lib
+
+
+@contextlib.contextmanager
+def using(library: ctypes.CDLL):
+    """Run the wrappers below against another build (the mutation tests)."""
+    global _lib
+    saved = lib()
+    _lib = library
+    try:
+        yield
+    finally:
+        _lib = saved
+
+
+def build_source(src_text: str, out_path: str) -> str:
+    """Compile C source text with the oracle's flags into `out_path`."""
+    src = out_path + ".c"
+    with open(src, "w") as f:
+        f.write(src_text)
+    subprocess.check_call(["gcc", *CFLAGS, "-o", out_path, src, "-lm"])
+    return out_path
+
+
+def source() -> str:
+    with open(_SRC) as f:
+        return f.read()
 
 
 # ---------------------------------------------------------------- helpers --
