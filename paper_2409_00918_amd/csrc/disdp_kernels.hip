@@ -47,6 +47,14 @@
 //   DISDP_WAVE_CONTIG 1: a wave's U groups are contiguous (U KiB per fp32
 //                     stream per wave); 0: strided by the block width
 //   DISDP_MIN_WAVES   launch-bounds hint: waves per SIMD to fit (0 = none)
+//   DISDP_BLOCKS_PER_CU  resident blocks per CU for the fused/aggregation
+//                     vector kernels (0 = as many as registers allow).
+//                     Enforced by reserving 1/k of the CU's LDS per block
+//                     (the kernels use no LDS).  With W + 3 16-byte loads in
+//                     flight per lane, 2-3 blocks (8-12 waves, ~135 KB in
+//                     flight per CU) stream fastest: more outstanding
+//                     requests cost DRAM efficiency, 1 block is too few.
+//                     The quantize kernel (one load per lane) is not capped.
 //   DISDP_XCD_CHUNK   0: block b takes tile b.  C > 0 (one tile per block):
 //                     the dispatcher deals blocks round-robin to the 8
 //                     XCDs, and XCD x takes the chunks x, x+8, x+16, ... of
@@ -73,6 +81,9 @@
 #endif
 #ifndef DISDP_MIN_WAVES
 #define DISDP_MIN_WAVES 0
+#endif
+#ifndef DISDP_BLOCKS_PER_CU
+#define DISDP_BLOCKS_PER_CU 3
 #endif
 #ifndef DISDP_XCD_CHUNK
 #define DISDP_XCD_CHUNK 0
@@ -503,6 +514,37 @@ __global__ DISDP_LAUNCH_BOUNDS void quantize_element_kernel(QuantizeArgs q)
 
 constexpr int kU = DISDP_UNROLL;
 
+// Dynamic LDS bytes a vector-kernel block reserves so that at most
+// DISDP_BLOCKS_PER_CU blocks fit on a CU (0 = no cap), cached per device.
+int occupancy_lds_bytes()
+{
+    if (DISDP_BLOCKS_PER_CU <= 0)
+        return 0;
+    static std::atomic<int> cached[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64)
+        return 0;
+    int b = cached[dev].load(std::memory_order_relaxed);
+    if (b == 0) {
+        int per_cu = 0, per_block = 0;
+        if (hipDeviceGetAttribute(&per_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor,
+                                  dev) != hipSuccess ||
+            hipDeviceGetAttribute(&per_block, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) !=
+                hipSuccess ||
+            per_cu <= 0) {
+            b = -1;  // unknown: launch without a cap
+        } else {
+            b = (per_cu / DISDP_BLOCKS_PER_CU) & ~1023;
+            if (b > per_block)
+                b = per_block;
+            if (b <= 0)
+                b = -1;
+        }
+        cached[dev].store(b, std::memory_order_relaxed);
+    }
+    return b > 0 ? b : 0;
+}
+
 int cu_count()
 {
     static std::atomic<int> cached[64];
@@ -519,10 +561,11 @@ int cu_count()
     return c;
 }
 
-// Blocks of `fn` that fit on one CU at once (registers decide it here),
-// cached per kernel.  Occupancy depends only on the kernel and the block
-// size, so one entry per kernel serves every device of one architecture.
-int resident_blocks_per_cu(const void *fn)
+// Blocks of `fn` that fit on one CU at once (registers, or the reserved
+// LDS), cached per kernel.  Occupancy depends only on the kernel, the block
+// size and the LDS reservation, which are fixed per process, so one entry
+// per kernel serves every device of one architecture.
+int resident_blocks_per_cu(const void *fn, int lds_bytes)
 {
     static std::mutex mu;
     static const void *keys[512];
@@ -533,7 +576,8 @@ int resident_blocks_per_cu(const void *fn)
         if (keys[i] == fn)
             return vals[i];
     int nb = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, fn, kBlock, 0) != hipSuccess || nb < 1)
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, fn, kBlock, lds_bytes) != hipSuccess ||
+        nb < 1)
         nb = 1;
     if (used < 512) {
         keys[used] = fn;
@@ -545,13 +589,14 @@ int resident_blocks_per_cu(const void *fn)
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-// `work_blocks`: blocks needed for one tile (or element chunk) each.
+// `work_blocks`: blocks needed for one tile (or element chunk) each;
+// `lds_bytes`: dynamic LDS reserved per block (an occupancy cap).
 hipError_t launch_kernel(const void *fn, int64_t work_blocks, bool persistent, const LaunchArgs &a,
-                         hipStream_t stream)
+                         hipStream_t stream, int lds_bytes = 0)
 {
     int64_t blocks = work_blocks;
     if (persistent) {
-        const int64_t cap = static_cast<int64_t>(cu_count()) * resident_blocks_per_cu(fn) *
+        const int64_t cap = static_cast<int64_t>(cu_count()) * resident_blocks_per_cu(fn, lds_bytes) *
                             DISDP_GRID_ROUNDS;
         if (blocks > cap)
             blocks = cap;
@@ -562,7 +607,8 @@ hipError_t launch_kernel(const void *fn, int64_t work_blocks, bool persistent, c
     if (blocks < 1)
         blocks = 1;
     void *args[] = {const_cast<LaunchArgs *>(&a)};
-    return hipLaunchKernel(fn, dim3(static_cast<unsigned>(blocks)), dim3(kBlock), args, 0, stream);
+    return hipLaunchKernel(fn, dim3(static_cast<unsigned>(blocks)), dim3(kBlock), args,
+                           static_cast<size_t>(lds_bytes), stream);
 }
 
 template <int W, int GT, int MODE, bool ADAM>
@@ -581,7 +627,7 @@ hipError_t launch_vector(const LaunchArgs &a, hipStream_t stream)
     }
 #endif
     return launch_kernel(reinterpret_cast<const void *>(&vector_kernel<W, GT, MODE, ADAM, U>),
-                         blocks, DISDP_GRID_MODE == 0, a, stream);
+                         blocks, DISDP_GRID_MODE == 0, a, stream, occupancy_lds_bytes());
 }
 
 template <int GT, int MODE, bool ADAM>
