@@ -102,14 +102,18 @@ def hparams(wl):
 
 
 def allocate(wl):
-    import torch
+    """The shard's arrays in one allocation placed by disdp_shard_layout
+    (as a parameter server would lay out its shard), filled with the seeded
+    step-1 inputs."""
+    import paper_2409_00918_amd as dd
     import synth
-    dg = synth.device_grads(wl.wid, 1, wl.W, wl.n, wl.sigma, gdtype=wl.gdtype,
-                            outlier_frac=wl.outlier_frac,
-                            outlier_scale=wl.outlier_scale)
-    dp, dm, dv = synth.device_state(wl.wid, wl.n, wl.p_sigma)
-    d16 = torch.empty(wl.n, dtype=torch.int16, device="cuda")
-    return dg, dp, dm, dv, d16
+    sh = dd.allocate_shard(wl.n, wl.W, wl.gdtype)
+    synth.device_grads(wl.wid, 1, wl.W, wl.n, wl.sigma, gdtype=wl.gdtype,
+                       outlier_frac=wl.outlier_frac, outlier_scale=wl.outlier_scale,
+                       out=sh.grads)
+    synth.device_state(wl.wid, wl.n, wl.p_sigma, out=(sh.param, sh.m, sh.v))
+    allocate.keep = sh               # the slab lives as long as the views are used
+    return sh.grads, sh.param, sh.m, sh.v, sh.param_bf16
 
 
 def copy_ceiling_gbps(elems=1 << 30, reps=10):
@@ -173,7 +177,6 @@ def run_bench(args):
     wl = synth.WORKLOADS[args.workload]
     torch.cuda.set_device(0)
     dd.lib()
-    dg, dp, dm, dv, d16 = allocate(wl)
     hp = hparams(wl)
     stream = torch.cuda.current_stream()
     contrib = "float"
@@ -182,12 +185,18 @@ def run_bench(args):
         # fused call sums int32 contributions (fixed mode at the shard's scale)
         if wl.mode != "fixed":
             raise SystemExit("--contributions i32 needs a fixed-point workload")
+        sh = dd.allocate_shard(wl.n, wl.W, "i32")
         for w in range(wl.W):
-            q = torch.empty(wl.n, dtype=torch.int32, device="cuda")
-            dd.quantize(dg[w], q, frac_bits=wl.frac_bits)
-            dg[w] = q
+            g = synth.device_grad(wl.wid, 1, w, wl.n, wl.sigma, wl.gdtype,
+                                  wl.outlier_frac, wl.outlier_scale)
+            dd.quantize(g, sh.grads[w], frac_bits=wl.frac_bits)
+            del g
+        synth.device_state(wl.wid, wl.n, wl.p_sigma, out=(sh.param, sh.m, sh.v))
         torch.cuda.synchronize()
+        dg, dp, dm, dv, d16 = sh.grads, sh.param, sh.m, sh.v, sh.param_bf16
         contrib = "int32"
+    else:
+        dg, dp, dm, dv, d16 = allocate(wl)
 
     def step(t):
         dd.aggregate_adam(dg, dp, dm, dv, d16, lr=hp["lr"], beta1=hp["beta1"],

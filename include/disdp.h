@@ -16,7 +16,9 @@
  *   disdp_aggregate_adam -- both in one pass over memory, with the bf16
  *                           parameter copy fused into the store;
  *   disdp_quantize       -- the worker-side conversion of a gradient into the
- *                           integer format the fixed-point mode sums.
+ *                           integer format the fixed-point mode sums;
+ *   disdp_shard_layout   -- where to place a shard's arrays in one
+ *                           allocation for the fastest streaming.
  *
  * The calls follow the shape of the paper's asynchronous push/pull API
  * (Table II: a buffer pointer and a length; completion awaited through a
@@ -181,6 +183,41 @@ disdp_status_t disdp_aggregate_adam(const void *const *grads, int W,
  * input). */
 disdp_status_t disdp_quantize(const void *grad, disdp_dtype_t gdtype, int64_t n,
                               int frac_bits, int32_t *out, hipStream_t stream);
+
+/* Optional arrays a shard layout reserves room for (bit flags). */
+enum {
+    DISDP_LAYOUT_BF16_COPY = 1, /* the bf16 parameter copy            */
+    DISDP_LAYOUT_AGG_F32 = 2,   /* an fp32 aggregate                  */
+    DISDP_LAYOUT_AGG_I32 = 4    /* an int32 aggregate (fixed mode)    */
+};
+
+/* Where to place the arrays of one shard -- the W contributions and the
+ * parameter server's 12-byte state and 2-byte copy (Section III-D, step 5)
+ * -- inside ONE device allocation so that the fused kernel streams them at
+ * its best and most repeatable rate.  The kernel walks every array in
+ * lockstep, and on MI355X how the arrays' starts sit relative to each other
+ * at 2 MiB granularity changes the streaming rate by several per cent:
+ * 4-byte arrays whose starts differ by an odd number of 2 MiB pages contend,
+ * an even number does not; for consecutive 2-byte arrays an odd number
+ * streamed fastest.  The arrays follow one another, each rounded up to
+ * whole pages and at least one unused page apart, with one more page
+ * skipped where needed so that every 4-byte array starts on an even page
+ * and a 2-byte array following a 2-byte array starts an odd number of pages
+ * after it.  Independent allocations land at arbitrary relative offsets
+ * and run slower and less repeatably.
+ * Pure computation: no HIP call, nothing allocated.
+ *   n, W, gdtype  the shard (1 <= W <= 64; gdtype F32, BF16 or I32).
+ *   flags         DISDP_LAYOUT_* arrays to include besides contributions and
+ *                 p, m, v.
+ *   offsets       caller array of W + 6 int64: byte offsets of
+ *                 contributions 0..W-1, then param, m, v, param_bf16,
+ *                 agg_f32, agg_i32 (-1 for arrays not requested).
+ *   total_bytes   bytes to allocate; the allocation must be 2 MiB aligned
+ *                 (hipMalloc's large allocations are).
+ * Returns DISDP_OK, or DISDP_ERR_INVALID_ARG / DISDP_ERR_UNSUPPORTED for a
+ * bad n, W, NULL output or unknown dtype. */
+disdp_status_t disdp_shard_layout(int64_t n, int W, disdp_dtype_t gdtype, unsigned flags,
+                                  int64_t *offsets, int64_t *total_bytes);
 
 /* A static, NUL-terminated English name for a status code (never NULL;
  * unknown codes give "unknown status"). */

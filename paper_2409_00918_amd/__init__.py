@@ -14,6 +14,8 @@ call raises.
 ``adam_step``       -- the optimizer step alone       (disdp_adam_step)
 ``aggregate_adam``  -- both in one pass               (disdp_aggregate_adam)
 ``quantize``        -- a worker's float -> int32 conversion (disdp_quantize)
+``allocate_shard``  -- one device allocation holding a shard's arrays, placed
+                       by disdp_shard_layout
 """
 from __future__ import annotations
 
@@ -31,7 +33,8 @@ AGG_FP32, AGG_FIXED = 0, 1
 MAX_W = 64
 
 EXPORTS = ("disdp_aggregate", "disdp_adam_step", "disdp_aggregate_adam",
-           "disdp_quantize", "disdp_status_string")
+           "disdp_quantize", "disdp_shard_layout", "disdp_status_string")
+LAYOUT_BF16_COPY, LAYOUT_AGG_F32, LAYOUT_AGG_I32 = 1, 2, 4
 
 
 class AdamWHParams(ctypes.Structure):
@@ -92,6 +95,8 @@ def lib() -> ctypes.CDLL:
                                            ctypes.POINTER(AdamWHParams), vp]
         L.disdp_quantize.restype = ci
         L.disdp_quantize.argtypes = [vp, ci, i64, ci, vp, vp]
+        L.disdp_shard_layout.restype = ci
+        L.disdp_shard_layout.argtypes = [i64, ci, ci, ctypes.c_uint, vp, vp]
         L.disdp_status_string.restype = ctypes.c_char_p
         L.disdp_status_string.argtypes = [ci]
         _lib = L
@@ -277,6 +282,56 @@ def quantize(grad, out, *, frac_bits: int, stream=None) -> None:
     st = raw_quantize(_dev_ptr(grad, "grad", n, allowed), gdt, n, frac_bits,
                       _dev_ptr(out, "out", n, (torch.int32,)), _stream(stream, grad))
     _check(st, "disdp_quantize")
+
+
+_GDT = {"f32": DT_F32, "bf16": DT_BF16, "i32": DT_I32}
+
+
+def shard_layout(n: int, W: int, gdtype="f32", *, bf16_copy=True, agg_f32=False,
+                 agg_i32=False):
+    """(byte offsets, total bytes) of a shard's arrays in one allocation, as
+    disdp_shard_layout places them.  Offsets are listed as contributions
+    0..W-1, param, m, v, param_bf16, agg_f32, agg_i32 (-1 = not included)."""
+    flags = ((LAYOUT_BF16_COPY if bf16_copy else 0) | (LAYOUT_AGG_F32 if agg_f32 else 0)
+             | (LAYOUT_AGG_I32 if agg_i32 else 0))
+    offs = (ctypes.c_int64 * (W + 6))()
+    total = ctypes.c_int64()
+    st = lib().disdp_shard_layout(n, W, _GDT.get(gdtype, gdtype), flags, offs,
+                                  ctypes.byref(total))
+    _check(st, "disdp_shard_layout")
+    return list(offs), total.value
+
+
+class Shard:
+    """A shard's arrays as torch views of one device allocation (`slab`):
+    grads (W tensors), param, m, v, and when requested param_bf16 (int16
+    bits), agg_f32, agg_i32.  Contents are uninitialised."""
+
+    def __init__(self, n: int, W: int, gdtype="f32", *, bf16_copy=True, agg_f32=False,
+                 agg_i32=False, device="cuda"):
+        torch = _torch()
+        offs, total = shard_layout(n, W, gdtype, bf16_copy=bf16_copy, agg_f32=agg_f32,
+                                   agg_i32=agg_i32)
+        self.slab = torch.empty(total, dtype=torch.uint8, device=device)
+
+        def view(i, dtype, esize):
+            if offs[i] < 0:
+                return None
+            return self.slab[offs[i]: offs[i] + n * esize].view(dtype)
+
+        gt, gsz = {"f32": (torch.float32, 4), "bf16": (torch.int16, 2),
+                   "i32": (torch.int32, 4)}[gdtype]
+        self.grads = [view(w, gt, gsz) for w in range(W)]
+        self.param = view(W, torch.float32, 4)
+        self.m = view(W + 1, torch.float32, 4)
+        self.v = view(W + 2, torch.float32, 4)
+        self.param_bf16 = view(W + 3, torch.int16, 2)
+        self.agg_f32 = view(W + 4, torch.float32, 4)
+        self.agg_i32 = view(W + 5, torch.int32, 4)
+
+
+def allocate_shard(n: int, W: int, gdtype="f32", **kw) -> Shard:
+    return Shard(n, W, gdtype, **kw)
 
 
 def algorithmic_bytes_per_element(W: int, grad_bytes: int, adam: bool = True,

@@ -276,6 +276,54 @@ disdp_status_t disdp_quantize(const void *grad, disdp_dtype_t gdtype, int64_t n,
     return disdp::launch_quantize(q, vec, stream) == hipSuccess ? DISDP_OK : DISDP_ERR_HIP;
 }
 
+disdp_status_t disdp_shard_layout(int64_t n, int W, disdp_dtype_t gdtype, unsigned flags,
+                                  int64_t *offsets, int64_t *total_bytes)
+{
+    if (n < 0 || n > kMaxN || W < 1 || W > disdp::kMaxW || !offsets || !total_bytes)
+        return DISDP_ERR_INVALID_ARG;
+    if (gdtype != DISDP_DT_F32 && gdtype != DISDP_DT_BF16 && gdtype != DISDP_DT_I32)
+        return DISDP_ERR_UNSUPPORTED;
+    constexpr int64_t kPage = int64_t(1) << 21;
+    auto pages = [](int64_t bytes) { return (bytes + kPage - 1) / kPage * kPage; };
+    // element size of each array in placement order; 0 = not requested
+    int esz[disdp::kMaxW + 6];
+    for (int w = 0; w < W; ++w)
+        esz[w] = grad_bytes(gdtype);
+    esz[W + 0] = 4;  // param
+    esz[W + 1] = 4;  // m
+    esz[W + 2] = 4;  // v
+    esz[W + 3] = (flags & DISDP_LAYOUT_BF16_COPY) ? 2 : 0;
+    esz[W + 4] = (flags & DISDP_LAYOUT_AGG_F32) ? 4 : 0;
+    esz[W + 5] = (flags & DISDP_LAYOUT_AGG_I32) ? 4 : 0;
+    // Arrays follow one another, page-rounded, at least one unused page
+    // apart; one more page is skipped when needed so that 4-byte arrays
+    // start on even pages (any two of them an even number of pages apart)
+    // and a 2-byte array following a 2-byte array starts an odd number of
+    // pages after it -- the placements that streamed fastest on MI355X.
+    int64_t at = 0;          // next free byte, page aligned
+    int64_t prev_start = -1;
+    int prev_esize = 0;
+    for (int i = 0; i < W + 6; ++i) {
+        const int esize = esz[i];
+        if (esize == 0) {
+            offsets[i] = -1;
+            continue;
+        }
+        if (prev_start >= 0)
+            at += kPage;
+        const int64_t page = at / kPage;
+        if (esize == 4 && (page & 1))
+            at += kPage;
+        else if (esize == 2 && prev_esize == 2 && !((page - prev_start / kPage) & 1))
+            at += kPage;
+        offsets[i] = at;
+        prev_start = at;
+        prev_esize = esize;
+        at += pages(n * esize);
+    }    *total_bytes = at;
+    return DISDP_OK;
+}
+
 const char *disdp_status_string(disdp_status_t status)
 {
     switch (status) {

@@ -122,25 +122,33 @@ def host_state(wid: int, n: int, p_sigma: float = 0.02,
 
 
 # ------------------------------------------------------------------- device --
+def device_grad(wid: int, step: int, w: int, n: int, sigma: float,
+                gdtype: str = "f32", outlier_frac: float = 0.0,
+                outlier_scale: float = 1.0, device="cuda"):
+    """Worker w's contribution as a device tensor (float32, or int16 bf16
+    bits), drawn by torch's device generator."""
+    import torch
+    gen = torch.Generator(device=device)
+    gen.manual_seed(seed_for(wid, step, w))
+    g = torch.randn(n, generator=gen, device=device, dtype=torch.float32)
+    g.mul_(sigma)
+    if outlier_frac > 0:
+        u = torch.rand(n, generator=gen, device=device, dtype=torch.float32)
+        g = torch.where(u < outlier_frac, g * outlier_scale, g)
+        del u
+    if gdtype == "bf16":
+        g = g.to(torch.bfloat16).view(torch.int16)
+    return g
+
+
 def device_grads(wid: int, step: int, W: int, n: int, sigma: float,
                  gdtype: str = "f32", outlier_frac: float = 0.0,
                  outlier_scale: float = 1.0, device="cuda", out=None):
-    """W contributions as device tensors (float32, or int16 bf16 bits),
-    drawn by torch's device generator.  ``out`` (a list of W tensors of the
-    right dtype and length) is refilled in place when given."""
-    import torch
+    """The W contributions (see device_grad).  ``out`` (a list of W tensors of
+    the right dtype and length) is refilled in place when given."""
     bufs = []
     for w in range(W):
-        gen = torch.Generator(device=device)
-        gen.manual_seed(seed_for(wid, step, w))
-        g = torch.randn(n, generator=gen, device=device, dtype=torch.float32)
-        g.mul_(sigma)
-        if outlier_frac > 0:
-            u = torch.rand(n, generator=gen, device=device, dtype=torch.float32)
-            g = torch.where(u < outlier_frac, g * outlier_scale, g)
-            del u
-        if gdtype == "bf16":
-            g = g.to(torch.bfloat16).view(torch.int16)
+        g = device_grad(wid, step, w, n, sigma, gdtype, outlier_frac, outlier_scale, device)
         if out is not None:
             out[w].copy_(g)
             del g
@@ -149,12 +157,20 @@ def device_grads(wid: int, step: int, W: int, n: int, sigma: float,
     return out if out is not None else bufs
 
 
-def device_state(wid: int, n: int, p_sigma: float = 0.02, device="cuda"):
+def device_state(wid: int, n: int, p_sigma: float = 0.02, device="cuda", out=None):
+    """(p, m, v) on the device: p ~ N(0, p_sigma), m = v = 0.  `out` (three
+    float32 tensors of length n) is filled in place when given."""
     import torch
     gen = torch.Generator(device=device)
     gen.manual_seed(seed_for(wid, 0, 1000))
     p = torch.randn(n, generator=gen, device=device, dtype=torch.float32)
     p.mul_(p_sigma)
+    if out is not None:
+        out[0].copy_(p)
+        del p
+        out[1].zero_()
+        out[2].zero_()
+        return tuple(out)
     m = torch.zeros(n, device=device, dtype=torch.float32)
     v = torch.zeros(n, device=device, dtype=torch.float32)
     return p, m, v

@@ -282,3 +282,52 @@ def test_int32_contributions_only_in_fixed_mode():
     # in fixed mode the combination passes the enumeration checks (and then
     # fails here only on the planted aliasing, so nothing launches)
     assert agg(gdtype=dd.DT_I32, mode=dd.AGG_FIXED, f32=A[2]) == dd.ERR_ALIAS
+
+
+# -------------------------------------------------------------- shard layout --
+PAGE = 1 << 21
+
+
+@pytest.mark.parametrize("n,W,gdt", [(875_000_000, 8, "f32"), (812_500_000, 16, "bf16"),
+                                     (2_734_375_000, 8, "i32"), (1, 1, "f32"), (0, 3, "bf16"),
+                                     (3_000_001, 64, "f32")])
+@pytest.mark.parametrize("opts", [dict(), dict(bf16_copy=False), dict(agg_f32=True, agg_i32=True)])
+def test_shard_layout_places_every_array_on_staggered_pages(n, W, gdt, opts):
+    offs, total = dd.shard_layout(n, W, gdt, **opts)
+    esize = {"f32": 4, "bf16": 2, "i32": 4}[gdt]
+    want = [n * esize] * W + [4 * n] * 3 + [
+        2 * n if opts.get("bf16_copy", True) else 0,
+        4 * n if opts.get("agg_f32") else 0, 4 * n if opts.get("agg_i32") else 0]
+    esizes = [esize] * W + [4, 4, 4, 2, 4, 4]
+    requested = [True] * (W + 3) + [opts.get("bf16_copy", True), bool(opts.get("agg_f32")),
+                                    bool(opts.get("agg_i32"))]
+    placed = [(o, sz, e) for o, sz, e in zip(offs, want, esizes) if o >= 0]
+    assert [o >= 0 for o in offs] == requested
+    prev_end = prev = None
+    for o, sz, e in placed:
+        assert o % PAGE == 0
+        rounded = -(-sz // PAGE) * PAGE
+        if prev_end is not None:
+            gap = (o - prev_end) // PAGE
+            assert gap in (1, 2)                 # one unused page, two to fix parity
+            if gap == 2:                         # the second page only when needed
+                assert (e == 4 and (o // PAGE - 1) % 2 == 1) or \
+                    (e == 2 and prev[1] == 2 and (o // PAGE - 1 - prev[0] // PAGE) % 2 == 0)
+        if e == 4:
+            assert (o // PAGE) % 2 == 0          # 4-byte arrays start on even pages
+        if e == 2 and prev is not None and prev[1] == 2:
+            assert ((o - prev[0]) // PAGE) % 2 == 1
+        prev_end, prev = o + rounded, (o, e)
+    assert total == prev_end
+
+
+def test_shard_layout_argument_checks():
+    L = dd.lib()
+    offs = (ctypes.c_int64 * 70)()
+    tot = ctypes.c_int64()
+    assert L.disdp_shard_layout(-1, 8, 0, 1, offs, ctypes.byref(tot)) == dd.ERR_INVALID_ARG
+    assert L.disdp_shard_layout(10, 0, 0, 1, offs, ctypes.byref(tot)) == dd.ERR_INVALID_ARG
+    assert L.disdp_shard_layout(10, 65, 0, 1, offs, ctypes.byref(tot)) == dd.ERR_INVALID_ARG
+    assert L.disdp_shard_layout(10, 8, 5, 1, offs, ctypes.byref(tot)) == dd.ERR_UNSUPPORTED
+    assert L.disdp_shard_layout(10, 8, 0, 1, None, ctypes.byref(tot)) == dd.ERR_INVALID_ARG
+    assert L.disdp_shard_layout(10, 8, 0, 1, offs, None) == dd.ERR_INVALID_ARG

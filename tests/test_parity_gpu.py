@@ -470,3 +470,31 @@ def test_pageable_host_memory_is_refused_before_any_launch():
     assert st == dd.ERR_INVALID_ARG
     st = dd.raw_quantize(pageable.ctypes.data, dd.DT_F32, n, 24, dev[0].data_ptr(), 0)
     assert st == dd.ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("W,gdtype,mode", [(8, "f32", "fp32"), (16, "bf16", "fp32"),
+                                           (4, "f32", "fixed")])
+def test_fused_on_a_shard_placed_by_the_layout_planner(W, gdtype, mode):
+    """All arrays as views of one allocation placed by disdp_shard_layout."""
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    n = 100_003
+    gs = synth.host_grads(600 + W, 1, W, n, 1e-4, gdtype=gdtype)
+    p, m, v = synth.host_state(600 + W, n, mv_sigma=1e-4)
+    sh = dd.allocate_shard(n, W, gdtype, agg_f32=True, agg_i32=(mode == "fixed"))
+    for dst, src in zip(sh.grads, gs):
+        dst.copy_(to_dev(src))
+    for dst, src in ((sh.param, p), (sh.m, m), (sh.v, v)):
+        dst.copy_(to_dev(src))
+    dd.aggregate_adam(sh.grads, sh.param, sh.m, sh.v, sh.param_bf16, lr=HP["lr"],
+                      beta1=HP["beta1"], beta2=HP["beta2"], eps=HP["eps"], weight_decay=HP["wd"],
+                      step=4, mode=mode, frac_bits=24, agg_out_f32=sh.agg_f32,
+                      agg_out_i32=sh.agg_i32)
+    t_.cuda.synchronize()
+    want = oracle.fused(gs, p, m, v, t=4, mode=oracle.AGG_FIXED if mode == "fixed" else oracle.AGG_FP32,
+                        frac_bits=24, want_agg_f32=True, want_agg_i32=(mode == "fixed"), **HP)
+    got = {"p": to_host(sh.param), "m": to_host(sh.m), "v": to_host(sh.v),
+           "p16": to_host(sh.param_bf16), "agg_f32": to_host(sh.agg_f32)}
+    if mode == "fixed":
+        got["agg_i32"] = to_host(sh.agg_i32)
+    assert_parity(got, want, f"shard W={W} {gdtype} {mode}")
