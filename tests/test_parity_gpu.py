@@ -244,6 +244,40 @@ def test_fused_equals_aggregate_then_adam_step(W, gdtype, mode):
         assert np.array_equal(to_host(x), to_host(y))
 
 
+@pytest.mark.parametrize("W,gdtype,mode", [(8, "f32", "fp32"), (16, "bf16", "fixed"),
+                                            (5, "f32", "fp32")])
+def test_chunked_calls_equal_one_call(W, gdtype, mode):
+    """Each element's result depends only on that element: the shard done in
+    one call equals the shard done as several calls on sub-ranges, whatever
+    the grid of each call and whether a sub-range starts on a vector
+    boundary (aligned chunks take the vector kernel, the others the element
+    kernel)."""
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    n = 3 * 262_144 + 4_099
+    gs = synth.host_grads(335, 2, W, n, 1e-4, gdtype=gdtype,
+                          outlier_frac=0.01, outlier_scale=100.0)
+    p, m, v = synth.host_state(335, n, mv_sigma=1e-4)
+    dg = [to_dev(g) for g in gs]
+    kw = dict(lr=HP["lr"], beta1=HP["beta1"], beta2=HP["beta2"], eps=HP["eps"],
+              weight_decay=HP["wd"], step=2, mode=mode, frac_bits=24)
+    ai_whole = t_.zeros(n, dtype=t_.int32, device="cuda") if mode == "fixed" else None
+    whole = [to_dev(x) for x in (p, m, v)] + [to_dev(np.zeros(n, np.uint16))]
+    dd.aggregate_adam(dg, *whole, agg_out_i32=ai_whole, **kw)
+    # cuts: one tile, a few groups, an odd element count, then the rest
+    cuts = [0, 1024, 1024 + 12, 1024 + 12 + 7, 262_144 + 5, n]
+    ai_parts = t_.zeros(n, dtype=t_.int32, device="cuda") if mode == "fixed" else None
+    parts = [to_dev(x) for x in (p, m, v)] + [to_dev(np.zeros(n, np.uint16))]
+    for lo, hi in zip(cuts[:-1], cuts[1:]):
+        dd.aggregate_adam([g[lo:hi] for g in dg], *(x[lo:hi] for x in parts),
+                          agg_out_i32=None if ai_parts is None else ai_parts[lo:hi], **kw)
+    t_.cuda.synchronize()
+    for x, y in zip(whole, parts):
+        assert np.array_equal(to_host(x), to_host(y))
+    if mode == "fixed":
+        assert np.array_equal(to_host(ai_whole), to_host(ai_parts))
+
+
 def test_empty_shard_writes_nothing():
     import paper_2409_00918_amd as dd
     t_ = torch()
