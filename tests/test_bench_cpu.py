@@ -1,0 +1,86 @@
+"""bench.py's host-side logic, on the CPU: the one-GPU guard, the committed
+counter records it reads, and the CPU-baseline leg on a tiny sample."""
+import json
+import os
+import re
+
+import numpy as np
+import pytest
+
+import bench
+import synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.mark.parametrize("argv,env", [(["--gpus", "2"], {}), (["--gpus", "8"], {}),
+                                      ([], {"WORLD_SIZE": "4"})])
+def test_more_than_one_gpu_exits_with_a_message(argv, env, monkeypatch, capsys):
+    for k, v in env.items():
+        monkeypatch.setenv(k, v)
+    assert bench.main(argv) == 2
+    assert "one GPU" in capsys.readouterr().err
+
+
+def test_kernel_source_hash_is_stable():
+    h = bench.kernel_source_hash()
+    assert re.fullmatch(r"[0-9a-f]{16}", h)
+    assert h == bench.kernel_source_hash()
+
+
+def _records():
+    out = []
+    for name in sorted(os.listdir(os.path.join(ROOT, "profiles"))):
+        if not name.startswith("counters_fused_"):
+            continue
+        with open(os.path.join(ROOT, "profiles", name)) as f:
+            for line in f:
+                m = re.match(r"\s*traffic-json:\s*(\{.*\})\s*$", line)
+                if m:
+                    out.append((name, json.loads(m.group(1))))
+    return out
+
+
+def test_committed_counter_records_are_consistent():
+    """Each committed record: read + write = total, the per-element figure is
+    total / N of its workload, and the measured HBM bytes are within 2% of the
+    algorithmic bytes (a kernel that re-read data would show more)."""
+    import paper_2409_00918_amd as dd
+    recs = _records()
+    assert recs, "no counter summaries under profiles/"
+    for name, r in recs:
+        wl = synth.WORKLOADS[r["workload"]]
+        assert name == f"counters_fused_{wl.name}.md"
+        assert r["read_bytes_per_launch"] + r["write_bytes_per_launch"] == r["bytes_per_launch"]
+        assert r["bytes_per_element"] == pytest.approx(r["bytes_per_launch"] / wl.n, abs=1e-3)
+        algo = dd.algorithmic_bytes_per_element(wl.W, 2 if wl.gdtype == "bf16" else 4)
+        assert abs(r["bytes_per_element"] / algo - 1) < 0.02, name
+        # per-dispatch KiB x scale reproduces the byte counts (scales are stored
+        # rounded to 5 decimals)
+        assert r["fetch_kib_per_dispatch"] * 1024 * r["fetch_scale"] == \
+            pytest.approx(r["read_bytes_per_launch"], rel=1e-4)
+        assert r["write_kib_per_dispatch"] * 1024 * r["write_scale"] == \
+            pytest.approx(r["write_bytes_per_launch"], rel=1e-4)
+
+
+def test_committed_traffic_is_tied_to_the_kernel_source():
+    recs = _records()
+    wl, h = recs[0][1]["workload"], recs[0][1]["kernel_source_hash"]
+    assert bench.committed_traffic(wl, h) is not None
+    assert bench.committed_traffic(wl, "0" * 16) is None
+    assert bench.committed_traffic("no_such_workload", h) is None
+
+
+def test_cpu_baseline_leg_on_a_tiny_sample(monkeypatch):
+    import torch
+    wl = synth.WORKLOADS["tiny_n1M_w4_f32"]
+    n = 4099
+    monkeypatch.setattr(bench, "CPU_SAMPLE", 2048)
+    monkeypatch.setattr(bench, "CPU_STEPS", 2)
+    gs = [torch.from_numpy(g) for g in synth.host_grads(wl.wid, 1, wl.W, n, wl.sigma)]
+    p, m, v = (torch.from_numpy(x) for x in synth.host_state(wl.wid, n))
+    r = bench.cpu_baseline(wl, gs, p, m, v)
+    assert r["kind"] == "oracle" and r["cores"] == 1 and r["unit"] == "G params/s"
+    assert r["value"] > 0 and "2048 elements" in r["sample"]
+    # the sample is read, not modified
+    assert np.array_equal(p.numpy(), synth.host_state(wl.wid, n)[0])
