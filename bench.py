@@ -18,7 +18,8 @@ Prints one JSON line.  ``roofline`` prices the kernel against HBM bandwidth
 (8 TB/s) with algorithmic bytes (each byte the call must move, counted once);
 ``traffic`` is the HBM byte count read from committed rocprofv3 counters when
 they were taken on the current kernel source, else null.  ``cpu_baseline``
-times the CPU oracle (single thread) on a bounded sample of the same shard.
+times the CPU oracle (single thread) on a bounded sample of the same shard;
+``cpu_baseline_threads`` the same sample split over the host's threads.
 """
 from __future__ import annotations
 
@@ -142,11 +143,24 @@ def copy_ceiling_gbps(elems=1 << 30, reps=10):
     return round(2 * elems * 4 / (ms * 1e-3) / 1e9, 1)
 
 
-def cpu_baseline(wl, dg, dp, dm, dv):
-    """The oracle, single-threaded, on the first CPU_SAMPLE elements of the
-    same shard for CPU_STEPS consecutive steps."""
+def host_threads() -> int:
+    """Host threads this process may use, at most 16."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+def cpu_baseline(wl, dg, dp, dm, dv, threads=1):
+    """The oracle on the first CPU_SAMPLE elements of the same shard for
+    CPU_STEPS consecutive steps.  threads > 1 splits the sample into that
+    many contiguous chunks, one oracle call per chunk and step on a thread
+    pool (the calls release the interpreter lock), as the paper's parameter
+    server spreads its CPU Adam over threads."""
     import numpy as np
     import oracle
+    from concurrent.futures import ThreadPoolExecutor
     ns = min(CPU_SAMPLE, wl.n)
     gs = []
     for g in dg:
@@ -155,15 +169,26 @@ def cpu_baseline(wl, dg, dp, dm, dv):
     p, m, v = (x[:ns].cpu().numpy() for x in (dp, dm, dv))
     hp = hparams(wl)
     mode = oracle.AGG_FIXED if wl.mode == "fixed" else oracle.AGG_FP32
-    t0 = time.perf_counter()
-    for t in range(1, CPU_STEPS + 1):
-        out = oracle.fused(gs, p, m, v, mode=mode, frac_bits=wl.frac_bits, t=t, **hp)
-        p, m, v = out["p"], out["m"], out["v"]
-    dt = time.perf_counter() - t0
+    cuts = [ns * k // threads for k in range(threads + 1)]
+    chunks = [(lo, hi) for lo, hi in zip(cuts[:-1], cuts[1:]) if hi > lo]
+    state = [(p[lo:hi], m[lo:hi], v[lo:hi]) for lo, hi in chunks]
+
+    def one(k, t):
+        lo, hi = chunks[k]
+        out = oracle.fused([g[lo:hi] for g in gs], *state[k], mode=mode,
+                           frac_bits=wl.frac_bits, t=t, **hp)
+        state[k] = (out["p"], out["m"], out["v"])
+
+    with ThreadPoolExecutor(max_workers=len(chunks)) as pool:
+        t0 = time.perf_counter()
+        for t in range(1, CPU_STEPS + 1):
+            list(pool.map(lambda k: one(k, t), range(len(chunks))))
+        dt = time.perf_counter() - t0
+    how = "single-threaded" if len(chunks) == 1 else f"{len(chunks)} threads, one chunk each"
     return {"value": round(ns * CPU_STEPS / dt / 1e9, 5),
-            "unit": "G params/s", "cores": 1, "kind": "oracle",
+            "unit": "G params/s", "cores": len(chunks), "kind": "oracle",
             "sample": f"first {ns} elements of the shard, {CPU_STEPS} consecutive "
-                      f"steps, single-threaded C oracle (gcc -O2), "
+                      f"steps, C oracle (gcc -O2), {how}, "
                       f"{dt:.1f} s on {platform.processor() or platform.machine()} "
                       f"({os.cpu_count()} host threads visible)"}
 
@@ -205,7 +230,11 @@ def run_bench(args):
                           stream=stream)
 
     # the oracle's sample is taken before any step, on the step-1 inputs
-    base = None if args.no_cpu_baseline else cpu_baseline(wl, dg, dp, dm, dv)
+    base = base_mt = None
+    if not args.no_cpu_baseline:
+        base = cpu_baseline(wl, dg, dp, dm, dv)
+        if host_threads() > 1:
+            base_mt = cpu_baseline(wl, dg, dp, dm, dv, threads=host_threads())
 
     t = 0
     for _ in range(args.warmup):
@@ -243,6 +272,8 @@ def run_bench(args):
                 "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBPS, 4),
                 "traffic": None if tr is None else tr["bytes_per_launch"],
+                "traffic_GBps": None if tr is None else
+                round(tr["bytes_per_launch"] / (avg_kernel_ms * 1e-3) / 1e9, 1),
                 "kernel": "vector_kernel (fused aggregate + AdamW)",
                 "algorithmic_bytes_per_element": bpe,
                 "avg_kernel_ms": round(avg_kernel_ms, 4),
@@ -275,6 +306,7 @@ def run_bench(args):
                    "parallelism": "single GPU, one shard"},
         "roofline": roofline,
         "cpu_baseline": base,
+        "cpu_baseline_threads": base_mt,
     }
     print(json.dumps(line), flush=True)
 

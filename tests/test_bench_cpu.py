@@ -84,3 +84,42 @@ def test_cpu_baseline_leg_on_a_tiny_sample(monkeypatch):
     assert r["value"] > 0 and "2048 elements" in r["sample"]
     # the sample is read, not modified
     assert np.array_equal(p.numpy(), synth.host_state(wl.wid, n)[0])
+
+
+def test_cpu_baseline_threads_cover_the_sample_like_one_call(monkeypatch):
+    """The threaded leg splits the sample into chunks; since every element is
+    independent its final state equals the single call's."""
+    import torch
+    import oracle
+    wl = synth.WORKLOADS["tiny_n1M_w4_f32"]
+    n = 5003
+    monkeypatch.setattr(bench, "CPU_SAMPLE", 4099)
+    monkeypatch.setattr(bench, "CPU_STEPS", 2)
+    calls = []
+    real = oracle.fused
+
+    def spy(gs, p, m, v, **kw):
+        out = real(gs, p, m, v, **kw)
+        calls.append((kw["t"], p.size, out["p"]))
+        return out
+
+    monkeypatch.setattr(oracle, "fused", spy)
+    gs = [torch.from_numpy(g) for g in synth.host_grads(wl.wid, 1, wl.W, n, wl.sigma)]
+    p, m, v = (torch.from_numpy(x) for x in synth.host_state(wl.wid, n))
+    r = bench.cpu_baseline(wl, gs, p, m, v, threads=3)
+    assert r["cores"] == 3 and "3 threads" in r["sample"]
+    sizes = sorted(s for t, s, _ in calls if t == 1)
+    assert sum(sizes) == 4099 and len(sizes) == 3
+    # the chunks' step-2 results laid end to end equal one call over the sample
+    ref = real([g[:4099].numpy() for g in gs], p[:4099].numpy(), m[:4099].numpy(),
+               v[:4099].numpy(), mode=oracle.AGG_FP32, frac_bits=0, t=1,
+               **bench.hparams(wl))
+    ref = real([g[:4099].numpy() for g in gs], ref["p"], ref["m"], ref["v"],
+               mode=oracle.AGG_FP32, frac_bits=0, t=2, **bench.hparams(wl))
+    got = [out for t, s, out in calls if t == 2]
+    assert len(got) == 3
+    # calls are recorded in completion order: look each expected chunk up
+    cuts = [4099 * k // 3 for k in range(4)]
+    want = [ref["p"][lo:hi] for lo, hi in zip(cuts[:-1], cuts[1:])]
+    for w in want:
+        assert any(g.size == w.size and np.array_equal(g, w) for g in got)
