@@ -212,8 +212,11 @@ enum {
  *   offsets       caller array of W + 6 int64: byte offsets of
  *                 contributions 0..W-1, then param, m, v, param_bf16,
  *                 agg_f32, agg_i32 (-1 for arrays not requested).
- *   total_bytes   bytes to allocate; the allocation must be 2 MiB aligned
- *                 (hipMalloc's large allocations are).
+ *   total_bytes   bytes to allocate.  Offsets are multiples of 2 MiB, so
+ *                 every array keeps the allocation's alignment (the vector
+ *                 kernels need 16 bytes; hipMalloc gives more).  Only the
+ *                 relative placement matters: moving a whole layout by
+ *                 whole pages streamed at the same rate.
  * Returns DISDP_OK, or DISDP_ERR_INVALID_ARG / DISDP_ERR_UNSUPPORTED for a
  * bad n, W, NULL output or unknown dtype. */
 disdp_status_t disdp_shard_layout(int64_t n, int W, disdp_dtype_t gdtype, unsigned flags,

@@ -186,14 +186,28 @@ def _dev_ptr(t, name: str, n: int, dtypes) -> int:
     return t.data_ptr()
 
 
-def _stream(stream, ref) -> int:
-    """The HIP stream to launch on: the one given, else torch's current
-    stream of `ref`'s device (of the current device for host tensors)."""
+def _device(tensors):
+    """The one GPU the device tensors among `tensors` live on (None when all
+    are pinned host memory); a call never spans devices."""
+    devs = {t.device for t in tensors if t is not None and t.is_cuda}
+    if len(devs) > 1:
+        raise ValueError("all device tensors of one call must be on one GPU, got "
+                         + ", ".join(sorted(str(d) for d in devs)))
+    return devs.pop() if devs else None
+
+
+def _launch(fn, tensors, stream, *args):
+    """Call `fn(*args, hip_stream)` with that GPU current: the library
+    launches on the current device.  The stream is the one given, else
+    torch's current stream of that device."""
     torch = _torch()
-    if stream is None:
-        dev = ref.device if ref.is_cuda else None
-        return torch.cuda.current_stream(dev).cuda_stream
-    return getattr(stream, "cuda_stream", stream)
+    dev = _device(tensors)
+    with torch.cuda.device(dev if dev is not None else torch.cuda.current_device()):
+        if stream is None:
+            s = torch.cuda.current_stream().cuda_stream
+        else:
+            s = getattr(stream, "cuda_stream", stream)
+        return fn(*args, s)
 
 
 def _hparams(lr, beta1, beta2, eps, weight_decay, step, grad_scale):
@@ -225,10 +239,10 @@ def aggregate(grads, *, mode="fp32", frac_bits: int = 0, agg_out_f32=None,
     length) into `agg_out_f32` and/or `agg_out_i32` (int32, fixed mode)."""
     torch = _torch()
     grads, ptrs, gdt, n = _grads(grads)
-    st = raw_aggregate(ptrs, len(grads), gdt, n, _mode(mode), frac_bits,
-                       _dev_ptr(agg_out_f32, "agg_out_f32", n, (torch.float32,)),
-                       _dev_ptr(agg_out_i32, "agg_out_i32", n, (torch.int32,)),
-                       _stream(stream, grads[0]))
+    st = _launch(raw_aggregate, grads + [agg_out_f32, agg_out_i32], stream,
+                 ptrs, len(grads), gdt, n, _mode(mode), frac_bits,
+                 _dev_ptr(agg_out_f32, "agg_out_f32", n, (torch.float32,)),
+                 _dev_ptr(agg_out_i32, "agg_out_i32", n, (torch.int32,)))
     _check(st, "disdp_aggregate")
 
 
@@ -238,13 +252,13 @@ def adam_step(grad, param, m, v, param_bf16_out=None, *, lr, beta1, beta2,
     torch = _torch()
     n = param.numel()
     f32 = (torch.float32,)
-    st = raw_adam_step(
+    st = _launch(
+        raw_adam_step, [grad, param, m, v, param_bf16_out], stream,
         _dev_ptr(grad, "grad", n, f32), _dev_ptr(param, "param", n, f32),
         _dev_ptr(m, "m", n, f32), _dev_ptr(v, "v", n, f32),
         _dev_ptr(param_bf16_out, "param_bf16_out", n,
                  (torch.bfloat16, torch.int16, torch.uint16)),
-        n, _hparams(lr, beta1, beta2, eps, weight_decay, step, grad_scale),
-        _stream(stream, param))
+        n, _hparams(lr, beta1, beta2, eps, weight_decay, step, grad_scale))
     _check(st, "disdp_adam_step")
 
 
@@ -256,7 +270,9 @@ def aggregate_adam(grads, param, m, v, param_bf16_out=None, *, lr, beta1,
     torch = _torch()
     grads, ptrs, gdt, n = _grads(grads)
     f32 = (torch.float32,)
-    st = raw_aggregate_adam(
+    st = _launch(
+        raw_aggregate_adam,
+        grads + [param, m, v, param_bf16_out, agg_out_f32, agg_out_i32], stream,
         ptrs, len(grads), gdt, n, _mode(mode), frac_bits,
         _dev_ptr(param, "param", n, f32), _dev_ptr(m, "m", n, f32),
         _dev_ptr(v, "v", n, f32),
@@ -264,8 +280,7 @@ def aggregate_adam(grads, param, m, v, param_bf16_out=None, *, lr, beta1,
                  (torch.bfloat16, torch.int16, torch.uint16)),
         _dev_ptr(agg_out_f32, "agg_out_f32", n, f32),
         _dev_ptr(agg_out_i32, "agg_out_i32", n, (torch.int32,)),
-        _hparams(lr, beta1, beta2, eps, weight_decay, step, grad_scale),
-        _stream(stream, grads[0]))
+        _hparams(lr, beta1, beta2, eps, weight_decay, step, grad_scale))
     _check(st, "disdp_aggregate_adam")
 
 
@@ -279,8 +294,9 @@ def quantize(grad, out, *, frac_bits: int, stream=None) -> None:
         raise TypeError("quantize takes float32 or bf16 input")
     allowed = (torch.float32,) if gdt == DT_F32 else \
         (torch.bfloat16, torch.int16, torch.uint16)
-    st = raw_quantize(_dev_ptr(grad, "grad", n, allowed), gdt, n, frac_bits,
-                      _dev_ptr(out, "out", n, (torch.int32,)), _stream(stream, grad))
+    st = _launch(raw_quantize, [grad, out], stream,
+                 _dev_ptr(grad, "grad", n, allowed), gdt, n, frac_bits,
+                 _dev_ptr(out, "out", n, (torch.int32,)))
     _check(st, "disdp_quantize")
 
 
@@ -331,6 +347,8 @@ class Shard:
 
 
 def allocate_shard(n: int, W: int, gdtype="f32", **kw) -> Shard:
+    """A Shard of n elements with W contributions of `gdtype` ("f32", "bf16"
+    or "i32"); keyword arguments as for Shard."""
     return Shard(n, W, gdtype, **kw)
 
 

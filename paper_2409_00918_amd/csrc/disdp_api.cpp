@@ -320,7 +320,8 @@ disdp_status_t disdp_shard_layout(int64_t n, int W, disdp_dtype_t gdtype, unsign
         prev_start = at;
         prev_esize = esize;
         at += pages(n * esize);
-    }    *total_bytes = at;
+    }
+    *total_bytes = at;
     return DISDP_OK;
 }
 

@@ -331,3 +331,19 @@ def test_shard_layout_argument_checks():
     assert L.disdp_shard_layout(10, 8, 5, 1, offs, ctypes.byref(tot)) == dd.ERR_UNSUPPORTED
     assert L.disdp_shard_layout(10, 8, 0, 1, None, ctypes.byref(tot)) == dd.ERR_INVALID_ARG
     assert L.disdp_shard_layout(10, 8, 0, 1, offs, None) == dd.ERR_INVALID_ARG
+
+
+def test_binding_refuses_a_call_spanning_two_gpus():
+    """The library launches on one device; the binding checks that every
+    device tensor of a call lives on the same GPU (stand-in objects: no GPU
+    is touched)."""
+    import types
+    import paper_2409_00918_amd as dd
+    import torch
+    g0 = types.SimpleNamespace(is_cuda=True, device=torch.device("cuda", 0))
+    g1 = types.SimpleNamespace(is_cuda=True, device=torch.device("cuda", 1))
+    host = types.SimpleNamespace(is_cuda=False, device=torch.device("cpu"))
+    assert dd._device([g0, None, host, g0]) == torch.device("cuda", 0)
+    assert dd._device([host, None]) is None
+    with pytest.raises(ValueError, match="one GPU"):
+        dd._device([g0, host, g1])
