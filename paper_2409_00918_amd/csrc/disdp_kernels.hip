@@ -102,7 +102,7 @@ namespace disdp {
 namespace {
 
 constexpr int kBlock = DISDP_BLOCK;
-constexpr int kWave = 64;
+[[maybe_unused]] constexpr int kWave = 64;  // used by DISDP_WAVE_CONTIG
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
@@ -415,7 +415,7 @@ __device__ __forceinline__ void process_element(const LaunchArgs &a, int64_t i)
 // ---- kernels -----------------------------------------------------------------
 
 // Tiles per XCD chunk for a shard of `n_tiles` full tiles (>= 1).
-__host__ __device__ __forceinline__ int64_t xcd_chunk(int64_t n_tiles)
+[[maybe_unused]] __host__ __device__ __forceinline__ int64_t xcd_chunk(int64_t n_tiles)
 {
     if (DISDP_XCD_CHUNK > 0)
         return DISDP_XCD_CHUNK;

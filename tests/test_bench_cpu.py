@@ -51,7 +51,9 @@ def test_committed_counter_records_are_consistent():
     for name, r in recs:
         wl = synth.WORKLOADS[r["workload"]]
         assert name == f"counters_fused_{wl.name}.md"
-        assert r["read_bytes_per_launch"] + r["write_bytes_per_launch"] == r["bytes_per_launch"]
+        # each of the three is rounded to whole bytes on its own
+        assert abs(r["read_bytes_per_launch"] + r["write_bytes_per_launch"]
+                   - r["bytes_per_launch"]) <= 2
         assert r["bytes_per_element"] == pytest.approx(r["bytes_per_launch"] / wl.n, abs=1e-3)
         algo = dd.algorithmic_bytes_per_element(wl.W, 2 if wl.gdtype == "bf16" else 4)
         assert abs(r["bytes_per_element"] / algo - 1) < 0.02, name
