@@ -13,6 +13,7 @@ lr 1e-4, betas (0.9, 0.95), eps 1e-8, weight decay 0.1.
     python bench.py [--steps K] [--warmup W] [--workload NAME]
     python bench.py --interference      # fused call next to a bf16 GEMM loop
     python bench.py --copy-probe        # plain 4 GiB device copy (counter scale)
+    python bench.py --entry aggregate   # another entry point on the same shard
 
 Prints one JSON line.  ``roofline`` prices the kernel against HBM bandwidth
 (8 TB/s) with algorithmic bytes (each byte the call must move, counted once);
@@ -410,6 +411,90 @@ def run_quantize(args):
                                    "algorithmic_bytes_per_element": gb + 4}}), flush=True)
 
 
+def run_entry(args):
+    """One entry point other than the fused call, on the same shard:
+    aggregate  -- disdp_aggregate: W contributions read, the aggregate
+                  written (fp32, or int32 in fixed mode);
+    adam_step  -- disdp_adam_step on an fp32 aggregate: 4 + 12 bytes read,
+                  12 + 2 written;
+    two_call   -- disdp_aggregate into an fp32 aggregate, then
+                  disdp_adam_step on it: the unfused path, 8 bytes per
+                  element more than the fused call."""
+    import numpy as np
+    import torch
+    import paper_2409_00918_amd as dd
+    import synth
+    wl = synth.WORKLOADS[args.workload]
+    torch.cuda.set_device(0)
+    dd.lib()
+    hp = hparams(wl)
+    fixed = wl.mode == "fixed"
+    gb = 2 if wl.gdtype == "bf16" else 4
+    kw = dict(lr=hp["lr"], beta1=hp["beta1"], beta2=hp["beta2"], eps=hp["eps"],
+              weight_decay=hp["wd"])
+    if args.entry == "adam_step":
+        sh = dd.allocate_shard(wl.n, 1, "f32")
+        # an aggregate-sized gradient: one draw at sqrt(W) times the spread
+        synth.device_grads(wl.wid, 1, 1, wl.n, wl.sigma * wl.W ** 0.5, out=sh.grads)
+        agg = sh.grads[0]
+        bpe = dd.algorithmic_bytes_per_element(1, 4)
+
+        def call(t):
+            dd.adam_step(agg, sh.param, sh.m, sh.v, sh.param_bf16, step=t, **kw)
+    else:
+        two = args.entry == "two_call"
+        sh = dd.allocate_shard(wl.n, wl.W, wl.gdtype, bf16_copy=two,
+                               agg_f32=two or not fixed, agg_i32=fixed and not two)
+        synth.device_grads(wl.wid, 1, wl.W, wl.n, wl.sigma, gdtype=wl.gdtype,
+                           outlier_frac=wl.outlier_frac, outlier_scale=wl.outlier_scale,
+                           out=sh.grads)
+        if two:
+            bpe = dd.algorithmic_bytes_per_element(wl.W, gb, adam=False, agg_f32=True) + \
+                dd.algorithmic_bytes_per_element(1, 4)
+
+            def call(t):
+                dd.aggregate(sh.grads, mode=wl.mode, frac_bits=wl.frac_bits,
+                             agg_out_f32=sh.agg_f32)
+                dd.adam_step(sh.agg_f32, sh.param, sh.m, sh.v, sh.param_bf16, step=t, **kw)
+        else:
+            bpe = dd.algorithmic_bytes_per_element(wl.W, gb, adam=False, agg_f32=not fixed,
+                                                   agg_i32=fixed)
+
+            def call(t):
+                dd.aggregate(sh.grads, mode=wl.mode, frac_bits=wl.frac_bits,
+                             agg_out_f32=None if fixed else sh.agg_f32,
+                             agg_out_i32=sh.agg_i32 if fixed else None)
+    if args.entry != "aggregate":
+        synth.device_state(wl.wid, wl.n, wl.p_sigma, out=(sh.param, sh.m, sh.v))
+    s = torch.cuda.current_stream()
+    t = 0
+    for _ in range(args.warmup):
+        t += 1
+        call(t)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    for a, b in ev:
+        t += 1
+        a.record(s)
+        call(t)
+        b.record(s)
+    torch.cuda.synchronize()
+    ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    achieved = wl.n * bpe / (ms * 1e-3) / 1e9
+    names = {"aggregate": "disdp_aggregate", "adam_step": "disdp_adam_step",
+             "two_call": "disdp_aggregate then disdp_adam_step"}
+    print(json.dumps({"metric": f"G elements/s ({names[args.entry]})",
+                      "value": round(wl.n / (ms * 1e-3) / 1e9, 3), "unit": "G elements/s",
+                      "avg_ms": round(ms, 4), "steps": args.steps,
+                      "config": {"workload": wl.name, "n": wl.n, "W": wl.W,
+                                 "grad_dtype": wl.gdtype, "aggregation": wl.mode},
+                      "roofline": {"bound": "hbm", "achieved": round(achieved, 1),
+                                   "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                                   "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                                   "algorithmic_bytes_per_element": bpe}}), flush=True)
+
+
 def _cu_mask_stream(first_cu: int, count: int, total: int):
     """A default-priority stream restricted to CUs [first_cu, first_cu+count)
     (hipExtStreamCreateWithCUMask on torch's HIP runtime), wrapped for torch."""
@@ -583,6 +668,9 @@ def main(argv=None):
                     help="p, m, v and the bf16 copy in pinned host memory")
     ap.add_argument("--contributions", choices=["float", "i32"], default="float",
                     help="i32: feed the fused call pre-quantised contributions")
+    ap.add_argument("--entry", choices=["fused", "aggregate", "adam_step", "two_call"],
+                    default="fused",
+                    help="time another entry point on the same shard (not the headline)")
     args = ap.parse_args(argv)
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus > 1 or world > 1:
@@ -598,6 +686,8 @@ def main(argv=None):
         run_quantize(args)
     elif args.host_state:
         run_host_state(args)
+    elif args.entry != "fused":
+        run_entry(args)
     else:
         run_bench(args)
     return 0

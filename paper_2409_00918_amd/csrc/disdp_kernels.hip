@@ -145,23 +145,24 @@ __device__ __forceinline__ uint32_t to_bf16(float x)
 }
 
 // Contribution -> int32 at scale 2^k: exact scaling, rint (ties to even),
-// saturation, NaN -> 0.
+// saturation, NaN -> 0.  Written without branches (selects only): the
+// rounded value is clamped in float to [-2^31, 2^31 - 128] -- no float lies
+// strictly between 2^31 - 128 and 2^31 -- so the conversion is always in
+// range and exact; values >= 2^31 then select INT32_MAX and NaN selects 0.
 __device__ __forceinline__ int32_t quantize(float x, float scale)
 {
     const float y = x * scale;
-    if (__builtin_isnan(y))
-        return 0;
     const float r = __builtin_rintf(y);
-    if (r >= 2147483648.0f)
-        return INT32_MAX;
-    if (r < -2147483648.0f)
-        return INT32_MIN;
-    return static_cast<int32_t>(r);
+    const float c = __builtin_fminf(__builtin_fmaxf(r, -2147483648.0f), 2147483520.0f);
+    int32_t q = static_cast<int32_t>(c);
+    q = r >= 2147483648.0f ? INT32_MAX : q;
+    return y != y ? 0 : q;
 }
 
 __device__ __forceinline__ int32_t saturate32(int64_t s)
 {
-    return s > INT32_MAX ? INT32_MAX : (s < INT32_MIN ? INT32_MIN : static_cast<int32_t>(s));
+    const int64_t hi = s > INT32_MAX ? int64_t(INT32_MAX) : s;
+    return static_cast<int32_t>(hi < INT32_MIN ? int64_t(INT32_MIN) : hi);
 }
 
 // One AdamW step on one element (decoupled decay, bias-corrected moments,

@@ -401,6 +401,63 @@ def test_quantize_matches_oracle(gdtype, k):
             assert np.array_equal(to_host(out), oracle.quantize_array(g, k)), (n, off)
 
 
+def _quantize_edge_values(k):
+    """Inputs at the edges of the integer format at scale 2^k: the largest
+    value below 2^31 and 2^31 itself after scaling, -2^31 and the next float
+    below it, ties to even around small integers, NaN, infinities, signed
+    zeros and denormals."""
+    s = np.float32(2.0 ** -k)
+    ints = np.array([2147483520.0, 2147483648.0, 2147483904.0, -2147483648.0,
+                     -2147483904.0, -2147483520.0, 0.5, 1.5, 2.5, -0.5, -1.5, -2.5,
+                     16777215.5, 8388607.5, 1.0, -1.0], np.float32)
+    vals = np.concatenate([ints * s,
+                           np.array([np.nan, -np.nan, np.inf, -np.inf, 0.0, -0.0, 1e-45,
+                                     -1e-45, 1e-38, 3e38, -3e38], np.float32)])
+    # neighbours one ulp either side of each scaled edge
+    near = np.concatenate([np.nextafter(vals, np.float32(np.inf)),
+                           np.nextafter(vals, np.float32(-np.inf))]).astype(np.float32)
+    return np.concatenate([vals, near[np.isfinite(near)]]).astype(np.float32)
+
+
+@pytest.mark.parametrize("k", [0, 24, 30])
+def test_quantize_and_fixed_aggregate_at_format_edges(k):
+    """The conversion's saturation, tie and NaN rules at the exact edges, in
+    disdp_quantize (fp32 and bf16 input) and inside the fused fixed-point
+    call, against the oracle."""
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    base = _quantize_edge_values(k)
+    rng = np.random.default_rng(900 + k)
+    n = 4 * base.size + 3                      # several groups and a ragged tail
+    g = base[rng.integers(0, base.size, n)]
+    g[:base.size] = base
+    out = to_dev(np.zeros(n, np.int32))
+    dd.quantize(to_dev(g), out, frac_bits=k)
+    t_.cuda.synchronize()
+    assert np.array_equal(to_host(out), oracle.quantize_array(g, k)), f"f32 k={k}"
+    gb = t_.from_numpy(g).to(t_.bfloat16).view(t_.int16).numpy().view(np.uint16)
+    dd.quantize(to_dev(gb), out, frac_bits=k)
+    t_.cuda.synchronize()
+    assert np.array_equal(to_host(out), oracle.quantize_array(gb, k)), f"bf16 k={k}"
+    # W = 3 contributions built from the edge values: saturated sums too
+    gs = [g, g[::-1].copy(), np.roll(g, 7)]
+    p, m, v = synth.host_state(901, n, mv_sigma=1e-3)
+    dg = [to_dev(x) for x in gs]
+    dp, dm, dv = to_dev(p), to_dev(m), to_dev(v)
+    d16 = to_dev(np.zeros(n, np.uint16))
+    dai = to_dev(np.zeros(n, np.int32))
+    daf = to_dev(np.zeros(n, np.float32))
+    dd.aggregate_adam(dg, dp, dm, dv, d16, lr=HP["lr"], beta1=HP["beta1"], beta2=HP["beta2"],
+                      eps=HP["eps"], weight_decay=HP["wd"], step=2, mode="fixed",
+                      frac_bits=k, agg_out_f32=daf, agg_out_i32=dai)
+    t_.cuda.synchronize()
+    want = oracle.fused(gs, p, m, v, mode=oracle.AGG_FIXED, frac_bits=k, t=2,
+                        want_agg_f32=True, want_agg_i32=True, **HP)
+    assert_parity({"p": to_host(dp), "m": to_host(dm), "v": to_host(dv), "p16": to_host(d16),
+                   "agg_f32": to_host(daf), "agg_i32": to_host(dai)}, want,
+                  f"fixed edges k={k}")
+
+
 @pytest.mark.parametrize("W", [1, 3, 8, 16, 20])
 def test_int32_contributions_match_oracle_and_float_path(W):
     import paper_2409_00918_amd as dd
