@@ -47,13 +47,19 @@
 //   DISDP_WAVE_CONTIG 1: a wave's U groups are contiguous (U KiB per fp32
 //                     stream per wave); 0: strided by the block width
 //   DISDP_MIN_WAVES   launch-bounds hint: waves per SIMD to fit (0 = none)
-//   DISDP_BLOCKS_PER_CU  resident blocks per CU for the fused/aggregation
-//                     vector kernels (0 = as many as registers allow).
-//                     Enforced by reserving 1/k of the CU's LDS per block
-//                     (the kernels use no LDS).  With W + 3 16-byte loads in
-//                     flight per lane, 2-3 blocks (8-12 waves, ~135 KB in
-//                     flight per CU) stream fastest: more outstanding
-//                     requests cost DRAM efficiency, 1 block is too few.
+//   DISDP_BLOCKS_PER_CU  resident blocks per CU for the fp32-mode fused and
+//                     aggregation vector kernels (0 = as many as registers
+//                     allow).  Enforced by reserving 1/k of the CU's LDS per
+//                     block (the kernels use no LDS).  With W + 3 16-byte
+//                     loads in flight per lane, 2-3 blocks (8-12 waves,
+//                     ~135 KB in flight per CU) stream fastest: more
+//                     outstanding requests cost DRAM efficiency, 1 block is
+//                     too few.
+//   DISDP_BLOCKS_PER_CU_FIXED  the same for fixed-point mode, whose lanes
+//                     spend ~4x more instructions per element converting
+//                     contributions and so need more resident waves to keep
+//                     loads in flight: 5 blocks (the aggregation +7%, the
+//                     fused call +2% over 3).
 //                     The quantize kernel (one load per lane) is not capped.
 //   DISDP_XCD_CHUNK   0: block b takes tile b.  C > 0 (one tile per block):
 //                     the dispatcher deals blocks round-robin to the 8
@@ -84,6 +90,9 @@
 #endif
 #ifndef DISDP_BLOCKS_PER_CU
 #define DISDP_BLOCKS_PER_CU 3
+#endif
+#ifndef DISDP_BLOCKS_PER_CU_FIXED
+#define DISDP_BLOCKS_PER_CU_FIXED 5
 #endif
 #ifndef DISDP_XCD_CHUNK
 #define DISDP_XCD_CHUNK 0
@@ -516,16 +525,17 @@ __global__ DISDP_LAUNCH_BOUNDS void quantize_element_kernel(QuantizeArgs q)
 constexpr int kU = DISDP_UNROLL;
 
 // Dynamic LDS bytes a vector-kernel block reserves so that at most
-// DISDP_BLOCKS_PER_CU blocks fit on a CU (0 = no cap), cached per device.
-int occupancy_lds_bytes()
+// `blocks_per_cu` blocks fit on a CU (0 = no cap), cached per device.
+int occupancy_lds_bytes(int blocks_per_cu)
 {
-    if (DISDP_BLOCKS_PER_CU <= 0)
+    constexpr int kMaxCap = 16;
+    if (blocks_per_cu <= 0 || blocks_per_cu > kMaxCap)
         return 0;
-    static std::atomic<int> cached[64];
+    static std::atomic<int> cached[64][kMaxCap + 1];
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64)
         return 0;
-    int b = cached[dev].load(std::memory_order_relaxed);
+    int b = cached[dev][blocks_per_cu].load(std::memory_order_relaxed);
     if (b == 0) {
         int per_cu = 0, per_block = 0;
         if (hipDeviceGetAttribute(&per_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor,
@@ -535,13 +545,13 @@ int occupancy_lds_bytes()
             per_cu <= 0) {
             b = -1;  // unknown: launch without a cap
         } else {
-            b = (per_cu / DISDP_BLOCKS_PER_CU) & ~1023;
+            b = (per_cu / blocks_per_cu) & ~1023;
             if (b > per_block)
                 b = per_block;
             if (b <= 0)
                 b = -1;
         }
-        cached[dev].store(b, std::memory_order_relaxed);
+        cached[dev][blocks_per_cu].store(b, std::memory_order_relaxed);
     }
     return b > 0 ? b : 0;
 }
@@ -627,8 +637,9 @@ hipError_t launch_vector(const LaunchArgs &a, hipStream_t stream)
         blocks = kXcds * ceil_div(ceil_div(n_tiles, c), kXcds) * c;
     }
 #endif
+    constexpr int cap = MODE == kAggFixed ? DISDP_BLOCKS_PER_CU_FIXED : DISDP_BLOCKS_PER_CU;
     return launch_kernel(reinterpret_cast<const void *>(&vector_kernel<W, GT, MODE, ADAM, U>),
-                         blocks, DISDP_GRID_MODE == 0, a, stream, occupancy_lds_bytes());
+                         blocks, DISDP_GRID_MODE == 0, a, stream, occupancy_lds_bytes(cap));
 }
 
 template <int GT, int MODE, bool ADAM>
