@@ -144,6 +144,18 @@ def copy_ceiling_gbps(elems=1 << 30, reps=10):
     return round(2 * elems * 4 / (ms * 1e-3) / 1e9, 1)
 
 
+def host_cpu_model() -> str:
+    """The host CPU's model name (from /proc/cpuinfo when readable)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
+
+
 def host_threads() -> int:
     """Host threads this process may use, at most 16."""
     try:
@@ -190,7 +202,7 @@ def cpu_baseline(wl, dg, dp, dm, dv, threads=1):
             "unit": "G params/s", "cores": len(chunks), "kind": "oracle",
             "sample": f"first {ns} elements of the shard, {CPU_STEPS} consecutive "
                       f"steps, C oracle (gcc -O2), {how}, "
-                      f"{dt:.1f} s on {platform.processor() or platform.machine()} "
+                      f"{dt:.1f} s on {host_cpu_model()} "
                       f"({os.cpu_count()} host threads visible)"}
 
 
@@ -278,6 +290,7 @@ def run_bench(args):
                 "kernel": "vector_kernel (fused aggregate + AdamW)",
                 "algorithmic_bytes_per_element": bpe,
                 "avg_kernel_ms": round(avg_kernel_ms, 4),
+                "median_kernel_ms": round(float(np.median(kernel_ms)), 4),
                 "min_kernel_ms": round(float(np.min(kernel_ms)), 4),
                 "kernel_source_hash": src_hash,
                 "copy_ceiling_GBps": copy_gbps,
