@@ -43,7 +43,10 @@
  *             the int32 aggregate is two's complement.
  * Asynchrony  Work is enqueued on `stream` (0 = the null stream) and the
  *             call returns at once; completion is the caller's
- *             hipStreamSynchronize or an event.
+ *             hipStreamSynchronize or an event.  A call enqueues kernel
+ *             launches only (no allocation, memset, copy or wait), so it
+ *             may be captured in a HIP graph; the hyperparameters, step t
+ *             included, are kernel arguments and are fixed at capture.
  * Alignment   Any alignment is accepted.  When every pointer is 16-byte
  *             aligned (8-byte for bf16 arrays) the vector kernels run,
  *             otherwise element-wise ones; results are identical.

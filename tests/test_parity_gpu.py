@@ -330,6 +330,56 @@ def test_side_stream_and_determinism():
         assert np.array_equal(x, y)
 
 
+@pytest.mark.parametrize("mode", ["fp32", "fixed"])
+def test_fused_call_captured_in_a_hip_graph(mode):
+    """The entry points enqueue only kernel launches (no allocation, memset
+    or synchronisation), so a caller can capture them in a HIP graph.  The
+    step's hyperparameters are kernel arguments fixed at capture.  Each of
+    three replays, with eager work and synchronisations between them, must
+    equal the same call made eagerly on a copy of the state."""
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    n, W = 1_000_003, 4
+    gs = synth.host_grads(345, 0, W, n, 1e-4, outlier_frac=0.01, outlier_scale=100.0)
+    p, m, v = synth.host_state(345, n, mv_sigma=1e-4)
+    dg = [to_dev(g) for g in gs]
+    cap = [to_dev(x) for x in (p, m, v)] + [to_dev(np.zeros(n, np.uint16))]
+    ref = [x.clone() for x in cap]
+    agg_cap = t_.zeros(n, dtype=t_.int32, device="cuda") if mode == "fixed" else None
+    agg_ref = t_.zeros(n, dtype=t_.int32, device="cuda") if mode == "fixed" else None
+    kw = dict(lr=HP["lr"], beta1=HP["beta1"], beta2=HP["beta2"], eps=HP["eps"],
+              weight_decay=HP["wd"], step=4, mode=mode, frac_bits=24)
+    t_.cuda.synchronize()
+    side = t_.cuda.Stream()
+    graph = t_.cuda.CUDAGraph()
+    with t_.cuda.graph(graph, stream=side):
+        dd.aggregate_adam(dg, *cap, agg_out_i32=agg_cap, **kw)
+    t_.cuda.synchronize()
+    # capture records the launch without running it
+    assert all(t_.equal(a, b) for a, b in zip(cap, ref))
+    other = t_.zeros(1 << 20, device="cuda")
+    for r in range(3):
+        graph.replay()
+        dd.aggregate_adam(dg, *ref, agg_out_i32=agg_ref, **kw)
+        t_.cuda.synchronize()
+        other.add_(1.0)                       # unrelated eager work between replays
+        t_.cuda.synchronize()
+        for a, b in zip(cap, ref):
+            assert t_.equal(a, b), f"replay {r}"
+        if mode == "fixed":
+            assert t_.equal(agg_cap, agg_ref), f"replay {r}: agg_i32"
+    want = oracle.fused(gs, p, m, v, mode=oracle.AGG_FIXED if mode == "fixed" else oracle.AGG_FP32,
+                        frac_bits=24, t=4, **HP)
+    # the first replay is one step from the initial state: check it against
+    # the oracle through a fresh eager call from the same start
+    fresh = [to_dev(x) for x in (p, m, v)] + [to_dev(np.zeros(n, np.uint16))]
+    dd.aggregate_adam(dg, *fresh, **kw)
+    t_.cuda.synchronize()
+    assert_parity({"p": to_host(fresh[0]), "m": to_host(fresh[1]), "v": to_host(fresh[2]),
+                   "p16": to_host(fresh[3])}, want, f"graph {mode}")
+    del graph
+
+
 def test_resume_from_saved_state_is_bit_identical():
     """5 steps straight equal 2 steps, a save/restore of (p, m, v, t), and 3
     more steps: all optimizer state is the caller's."""
