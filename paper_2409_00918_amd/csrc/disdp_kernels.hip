@@ -55,6 +55,12 @@
 //                     ~135 KB in flight per CU) stream fastest: more
 //                     outstanding requests cost DRAM efficiency, 1 block is
 //                     too few.
+//   DISDP_BLOCKS_PER_CU_SMALL  the cap for fp32-mode kernels whose lanes keep
+//                     at most DISDP_SMALL_LANE_BYTES of loads in flight
+//                     (W <= 2 fp32 contributions with the optimizer, the
+//                     optimizer step alone): fewer bytes per wave need one
+//                     more block per CU (+1.5 to +3% at cap 4; W = 4 and
+//                     larger are best at 3).
 //   DISDP_BLOCKS_PER_CU_FIXED  the same for fixed-point mode, whose lanes
 //                     spend ~4x more instructions per element converting
 //                     contributions and so need more resident waves to keep
@@ -93,6 +99,12 @@
 #endif
 #ifndef DISDP_BLOCKS_PER_CU_FIXED
 #define DISDP_BLOCKS_PER_CU_FIXED 5
+#endif
+#ifndef DISDP_BLOCKS_PER_CU_SMALL
+#define DISDP_BLOCKS_PER_CU_SMALL 4
+#endif
+#ifndef DISDP_SMALL_LANE_BYTES
+#define DISDP_SMALL_LANE_BYTES 80
 #endif
 #ifndef DISDP_XCD_CHUNK
 #define DISDP_XCD_CHUNK 0
@@ -677,7 +689,13 @@ hipError_t launch_vector(const LaunchArgs &a, hipStream_t stream)
         blocks = kXcds * ceil_div(ceil_div(n_tiles, c), kXcds) * c;
     }
 #endif
-    constexpr int base = MODE == kAggFixed ? DISDP_BLOCKS_PER_CU_FIXED : DISDP_BLOCKS_PER_CU;
+    // bytes of loads one lane keeps in flight: 4 elements of each
+    // contribution, plus p, m and v with the optimizer
+    constexpr int kGradBytes = GT == kGradBF16 ? 2 : 4;
+    constexpr int kLaneBytes = W > 0 ? 4 * (W * kGradBytes + (ADAM ? 12 : 0)) : 1 << 30;
+    constexpr int base = MODE == kAggFixed ? DISDP_BLOCKS_PER_CU_FIXED
+                         : kLaneBytes <= DISDP_SMALL_LANE_BYTES ? DISDP_BLOCKS_PER_CU_SMALL
+                                                                : DISDP_BLOCKS_PER_CU;
     return launch_kernel(reinterpret_cast<const void *>(&vector_kernel<W, GT, MODE, ADAM, U>),
                          blocks, DISDP_GRID_MODE == 0, a, stream,
                          occupancy_lds_bytes(blocks_per_cu_cap(base, stream)));
