@@ -380,6 +380,56 @@ def test_fused_call_captured_in_a_hip_graph(mode):
     del graph
 
 
+def _cu_masked_stream(n_cus):
+    """A default-priority stream restricted to the first n_cus CUs
+    (hipExtStreamCreateWithCUMask on torch's HIP runtime)."""
+    import ctypes
+    t_ = torch()
+    total = t_.cuda.get_device_properties(0).multi_processor_count
+    hip = ctypes.CDLL("libamdhip64.so.7")          # torch's runtime, already loaded
+    words = (total + 31) // 32
+    mask = (ctypes.c_uint32 * words)()
+    for cu in range(min(n_cus, total)):
+        mask[cu // 32] |= 1 << (cu % 32)
+    h = ctypes.c_void_p()
+    assert hip.hipExtStreamCreateWithCUMask(ctypes.byref(h), ctypes.c_uint32(words), mask) == 0
+    return t_.cuda.ExternalStream(h.value), h, hip
+
+
+@pytest.mark.parametrize("mode", ["fp32", "fixed"])
+def test_fused_on_cu_masked_streams(mode):
+    """On a CU-masked stream the library raises its per-CU occupancy cap
+    (a different launch configuration); results stay identical to the
+    default stream's and to the oracle."""
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    n, W = 2_000_003, 8
+    gs = synth.host_grads(346, 0, W, n, 1e-4, outlier_frac=0.01, outlier_scale=100.0)
+    p, m, v = synth.host_state(346, n, mv_sigma=1e-4)
+    dg = [to_dev(g) for g in gs]
+    kw = dict(lr=HP["lr"], beta1=HP["beta1"], beta2=HP["beta2"], eps=HP["eps"],
+              weight_decay=HP["wd"], step=2, mode=mode, frac_bits=24)
+    base = [to_dev(x) for x in (p, m, v)] + [to_dev(np.zeros(n, np.uint16))]
+    dd.aggregate_adam(dg, *base, **kw)
+    t_.cuda.synchronize()
+    want = oracle.fused(gs, p, m, v, mode=oracle.AGG_FIXED if mode == "fixed" else oracle.AGG_FP32,
+                        frac_bits=24, t=2, **HP)
+    assert_parity({"p": to_host(base[0]), "m": to_host(base[1]), "v": to_host(base[2]),
+                   "p16": to_host(base[3])}, want, f"default stream {mode}")
+    for n_cus in (32, 200):
+        s, h, hip = _cu_masked_stream(n_cus)
+        try:
+            st = [to_dev(x) for x in (p, m, v)] + [to_dev(np.zeros(n, np.uint16))]
+            t_.cuda.synchronize()
+            dd.aggregate_adam(dg, *st, stream=s, **kw)
+            s.synchronize()
+            for a, b in zip(base, st):
+                assert t_.equal(a, b), f"{n_cus} CUs, {mode}"
+        finally:
+            t_.cuda.synchronize()
+            hip.hipStreamDestroy(h)
+
+
 def test_resume_from_saved_state_is_bit_identical():
     """5 steps straight equal 2 steps, a save/restore of (p, m, v, t), and 3
     more steps: all optimizer state is the caller's."""
