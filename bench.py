@@ -106,7 +106,8 @@ def hparams(wl):
 def allocate(wl):
     """The shard's arrays in one allocation placed by disdp_shard_layout
     (as a parameter server would lay out its shard), filled with the seeded
-    step-1 inputs."""
+    step-1 inputs.  The returned Shard owns the allocation; its fields are
+    views into it."""
     import paper_2409_00918_amd as dd
     import synth
     sh = dd.allocate_shard(wl.n, wl.W, wl.gdtype)
@@ -114,8 +115,7 @@ def allocate(wl):
                        outlier_frac=wl.outlier_frac, outlier_scale=wl.outlier_scale,
                        out=sh.grads)
     synth.device_state(wl.wid, wl.n, wl.p_sigma, out=(sh.param, sh.m, sh.v))
-    allocate.keep = sh               # the slab lives as long as the views are used
-    return sh.grads, sh.param, sh.m, sh.v, sh.param_bf16
+    return sh
 
 
 def copy_ceiling_gbps(elems=1 << 30, reps=10):
@@ -234,7 +234,8 @@ def run_bench(args):
         dg, dp, dm, dv, d16 = sh.grads, sh.param, sh.m, sh.v, sh.param_bf16
         contrib = "int32"
     else:
-        dg, dp, dm, dv, d16 = allocate(wl)
+        sh = allocate(wl)
+        dg, dp, dm, dv, d16 = sh.grads, sh.param, sh.m, sh.v, sh.param_bf16
 
     def step(t):
         dd.aggregate_adam(dg, dp, dm, dv, d16, lr=hp["lr"], beta1=hp["beta1"],
@@ -542,7 +543,8 @@ def run_interference(args):
     wl = synth.WORKLOADS[DEFAULT_WORKLOAD]
     torch.cuda.set_device(0)
     dd.lib()
-    dg, dp, dm, dv, d16 = allocate(wl)
+    sh = allocate(wl)
+    dg, dp, dm, dv, d16 = sh.grads, sh.param, sh.m, sh.v, sh.param_bf16
     hp = hparams(wl)
     gen = torch.Generator(device="cuda")
     gen.manual_seed(synth.seed_for(4, 0, 2000))
