@@ -47,9 +47,13 @@
  *             launches only (no allocation, memset, copy or wait), so it
  *             may be captured in a HIP graph; the hyperparameters, step t
  *             included, are kernel arguments and are fixed at capture.
- * Alignment   Any alignment is accepted.  When every pointer is 16-byte
- *             aligned (8-byte for bf16 arrays) the vector kernels run,
- *             otherwise element-wise ones; results are identical.
+ * Alignment   Any alignment is accepted; results never depend on it.  The
+ *             vector kernels run when every array starts the same number of
+ *             elements past a 4-element boundary (16 bytes for 4-byte
+ *             arrays, 8 for bf16), e.g. any sub-range of aligned arrays: the
+ *             first few elements (up to 63, reaching a common 64-element
+ *             boundary when the arrays agree that far) are done one by one.
+ *             Otherwise an element-wise kernel runs.
  * Errors      Arguments are checked on the host in this order: counts and
  *             enumerations, hyperparameters, then (only when n > 0) NULL
  *             pointers, overlap, and -- the first HIP call -- that every

@@ -28,9 +28,6 @@ bool overlaps(Span a, Span b) { return a.lo < b.hi && b.lo < a.hi; }
 
 int grad_bytes(int gdtype) { return gdtype == DISDP_DT_BF16 ? 2 : 4; }
 
-// Alignment the vector kernels need for a contribution buffer: 4 elements.
-uintptr_t grad_vector_align(int gdtype) { return gdtype == DISDP_DT_BF16 ? 8 : 16; }
-
 // Largest n accepted: keeps every byte count far below 2^63.
 constexpr int64_t kMaxN = int64_t(1) << 56;
 
@@ -84,11 +81,6 @@ disdp::StepScalars step_scalars(const disdp_adamw_hparams_t *hp)
     return s;
 }
 
-bool aligned(const void *p, uintptr_t a)
-{
-    return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0;
-}
-
 // True when the GPU can dereference `p` at that very address: device or
 // managed memory, or pinned host memory mapped for the device at the same
 // address (hipHostMalloc).  Pageable host memory and unknown addresses are
@@ -110,6 +102,40 @@ bool gpu_addressable(const void *p)
     default:
         return false;
     }
+}
+
+// Elements to do one by one before the vector kernels can take arrays
+// `p[0..np)` of element sizes `esz`: 0 when all are aligned to 64 elements
+// (or to 4 elements but not all to 64), the distance to the next common
+// 64- or 4-element boundary when they share a phase, -1 when they do not
+// (or an array is not aligned to its own element size).  Never more than n.
+int common_head(const void *const *p, const int *esz, int np, int64_t n)
+{
+    int ph64 = -1;
+    bool same64 = true, same4 = true;
+    int ph4 = -1;
+    for (int i = 0; i < np; ++i) {
+        const uintptr_t u = reinterpret_cast<uintptr_t>(p[i]);
+        if (u % esz[i])
+            return -1;
+        const int e = static_cast<int>((u / esz[i]) & 63);
+        if (ph64 < 0) {
+            ph64 = e;
+            ph4 = e & 3;
+        }
+        same64 = same64 && e == ph64;
+        same4 = same4 && (e & 3) == ph4;
+    }
+    if (np == 0)
+        return 0;
+    int64_t head;
+    if (same64)
+        head = (64 - ph64) & 63;
+    else if (same4)
+        head = (4 - ph4) & 3;
+    else
+        return -1;
+    return static_cast<int>(head < n ? head : n);
 }
 
 // Shared body of the three entry points.  `adam` selects the optimizer;
@@ -195,16 +221,42 @@ disdp_status_t run(const void *const *grads, int W, int gdtype, int64_t n,
     if (adam)
         a.s = step_scalars(hp);
 
-    // Vector kernels move 4 elements per lane: 16-byte fp32 groups and
-    // 8-byte bf16 groups.
-    bool vec = true;
-    for (int w = 0; w < W; ++w)
-        vec = vec && aligned(grads[w], grad_vector_align(gdtype));
-    for (const void *p : {static_cast<const void *>(param), static_cast<const void *>(m),
-                          static_cast<const void *>(v), static_cast<const void *>(agg_f32),
-                          static_cast<const void *>(agg_i32)})
-        vec = vec && aligned(p, 16);
-    vec = vec && aligned(p16, 8);
+    // Vector kernels move 4 elements per lane: 16-byte groups of 4-byte
+    // arrays, 8-byte groups of 2-byte arrays.  Arrays that all start the same
+    // number of elements past such a boundary (a sub-range of aligned arrays)
+    // take the vector kernel too: their first elements are done one by one
+    // and the pointers advanced.  When the arrays agree modulo 64 elements
+    // the pointers are advanced to a 64-element boundary, which starts every
+    // array on a whole cache line (256 B for 4-byte arrays, 128 B for 2-byte
+    // ones): a wave's stores then cover whole lines, as for aligned arrays.
+    const void *ptrs[disdp::kMaxW + 6];
+    int sizes[disdp::kMaxW + 6];
+    int np = 0;
+    for (int w = 0; w < W; ++w) {
+        ptrs[np] = grads[w];
+        sizes[np++] = gb;
+    }
+    const void *outs_p[] = {param, m, v, p16, agg_f32, agg_i32};
+    const int outs_sz[] = {4, 4, 4, 2, 4, 4};
+    for (int k = 0; k < 6; ++k)
+        if (outs_p[k]) {
+            ptrs[np] = outs_p[k];
+            sizes[np++] = outs_sz[k];
+        }
+    const int head = common_head(ptrs, sizes, np, n);
+    const bool vec = head >= 0;
+    if (head > 0) {
+        a.head = head;
+        a.n = n - head;
+        for (int w = 0; w < W; ++w)
+            a.g[w] = static_cast<const char *>(grads[w]) + static_cast<int64_t>(head) * gb;
+        a.p = param ? param + head : nullptr;
+        a.m = m ? m + head : nullptr;
+        a.v = v ? v + head : nullptr;
+        a.p16 = p16 ? p16 + head : nullptr;
+        a.agg_f32 = agg_f32 ? agg_f32 + head : nullptr;
+        a.agg_i32 = agg_i32 ? agg_i32 + head : nullptr;
+    }
 
     hipError_t e = disdp::launch(a, adam ? disdp::kAggregateAdam : disdp::kAggregateOnly,
                                  vec, stream);
@@ -270,9 +322,21 @@ disdp_status_t disdp_quantize(const void *grad, disdp_dtype_t gdtype, int64_t n,
     q.g = grad;
     q.out = out;
     q.n = n;
+    q.head = 0;
     q.gdtype = gdtype;
     q.qscale = std::ldexp(1.0f, frac_bits);
-    const bool vec = aligned(grad, grad_vector_align(gdtype)) && aligned(out, 16);
+    // as in run(): a common misalignment is peeled off one element at a time
+    const int gb = grad_bytes(gdtype);
+    const void *ptrs[2] = {grad, out};
+    const int sizes[2] = {gb, 4};
+    const int head = common_head(ptrs, sizes, 2, n);
+    const bool vec = head >= 0;
+    if (head > 0) {
+        q.head = head;
+        q.n = n - head;
+        q.g = static_cast<const char *>(grad) + static_cast<int64_t>(head) * gb;
+        q.out = out + head;
+    }
     return disdp::launch_quantize(q, vec, stream) == hipSuccess ? DISDP_OK : DISDP_ERR_HIP;
 }
 

@@ -448,7 +448,8 @@ __device__ __forceinline__ void process_element(const LaunchArgs &a, int64_t i)
 // Vector kernel.  W > 0: compile-time worker count, U groups per lane;
 // W == 0: run-time worker count, one group per lane.  Groups [0, n/4) go
 // grid-stride in tiles of kBlock*U groups; the groups after the last full
-// tile go one per lane; the last n % 4 elements go to lanes of block 0.
+// tile go one per lane; the last n % 4 elements and the a.head elements
+// before the (vector-aligned) pointers go to lanes of block 0.
 template <int W, int GT, int MODE, bool ADAM, int U>
 __global__ DISDP_LAUNCH_BOUNDS void vector_kernel(LaunchArgs a)
 {
@@ -490,6 +491,9 @@ __global__ DISDP_LAUNCH_BOUNDS void vector_kernel(LaunchArgs a)
     }
     if (blockIdx.x == 0 && threadIdx.x < (a.n & 3))
         process_element<GT, MODE, ADAM>(a, (n_groups << 2) + threadIdx.x);
+    // the elements before the vector-aligned pointers
+    if (blockIdx.x == 0 && threadIdx.x < a.head)
+        process_element<GT, MODE, ADAM>(a, static_cast<int64_t>(threadIdx.x) - a.head);
 }
 
 // Element-wise kernel for buffers that are not vector aligned.
@@ -520,6 +524,10 @@ __global__ DISDP_LAUNCH_BOUNDS void quantize_vector_kernel(QuantizeArgs q)
     }
     if (blockIdx.x == 0 && threadIdx.x < (q.n & 3)) {
         const int64_t i = (n_groups << 2) + threadIdx.x;
+        q.out[i] = quantize(load_one<GT>(q.g, i), q.qscale);
+    }
+    if (blockIdx.x == 0 && threadIdx.x < q.head) {
+        const int64_t i = static_cast<int64_t>(threadIdx.x) - q.head;
         q.out[i] = quantize(load_one<GT>(q.g, i), q.qscale);
     }
 }

@@ -29,7 +29,9 @@ struct LaunchArgs {
     uint16_t *p16;         // bf16 parameter copy, may be NULL
     float *agg_f32;        // optional fp32 aggregate
     int32_t *agg_i32;      // optional int32 aggregate (fixed mode)
-    int64_t n;
+    int64_t n;             // elements from the pointers on
+    int head;              // 0-63 elements just before the pointers, done one
+                           // by one (pointers advanced to vector alignment)
     int W, gdtype, mode, frac_bits;
     float qscale, dqscale; // 2^k and 2^-k (fixed mode)
     StepScalars s;
@@ -45,6 +47,7 @@ struct QuantizeArgs {
     const void *g;     // n elements of gdtype (kGradF32 or kGradBF16)
     int32_t *out;      // n int32
     int64_t n;
+    int head;          // as in LaunchArgs
     int gdtype;
     float qscale;      // 2^k
 };

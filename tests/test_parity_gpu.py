@@ -63,6 +63,47 @@ def test_fused_unaligned_pointers(offsets, gdtype, mode):
         assert_parity(got, want, _label(offsets=offsets, n=n))
 
 
+@pytest.mark.parametrize("k", [1, 2, 3, 37, 63])
+@pytest.mark.parametrize("gdtype,mode", [("f32", "fp32"), ("bf16", "fixed"), ("bf16", "fp32"),
+                                         ("f32", "fixed")])
+def test_fused_common_misalignment(k, gdtype, mode):
+    """Every array starts k elements past a 64-element boundary (a sub-range
+    of aligned arrays): the library does the first 64 - k elements one by one
+    and runs the vector kernel on the rest.  Lengths shorter than that head
+    included."""
+    for n in (1, 2, 3, 4, 5, 26, 27, 28, 63, 64, 65, 1027, 40_001, 262_147):
+        got, want = run_fused_case(8, gdtype, mode, n, t=3, offsets=(k, k), seed=11 + k)
+        assert_parity(got, want, _label(k=k, gdtype=gdtype, mode=mode, n=n))
+
+
+@pytest.mark.parametrize("k", [1, 2, 3, 50])
+def test_aggregate_and_adam_step_common_misalignment(k):
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    for n in (2, 7, 70_001):
+        gs = synth.host_grads(360 + k, 1, 5, n, 1e-4, outlier_frac=0.01, outlier_scale=100.0)
+        dg = [to_dev(g, k) for g in gs]
+        af = to_dev(np.zeros(n, np.float32), k)
+        ai = to_dev(np.zeros(n, np.int32), k)
+        dd.aggregate(dg, mode="fixed", frac_bits=24, agg_out_f32=af, agg_out_i32=ai)
+        t_.cuda.synchronize()
+        want_i, want_f = oracle.aggregate_fixed(gs, 24)
+        assert np.array_equal(to_host(ai), want_i), (k, n)
+        assert f32_same(to_host(af), want_f), (k, n)
+        dd.aggregate(dg, mode="fp32", agg_out_f32=af)
+        t_.cuda.synchronize()
+        assert f32_same(to_host(af), oracle.aggregate_f32(gs)), (k, n)
+        p, m, v = synth.host_state(360 + k, n, mv_sigma=1e-4)
+        dp, dm, dv = to_dev(p, k), to_dev(m, k), to_dev(v, k)
+        d16 = to_dev(np.zeros(n, np.uint16), k)
+        dd.adam_step(af, dp, dm, dv, d16, lr=HP["lr"], beta1=HP["beta1"], beta2=HP["beta2"],
+                     eps=HP["eps"], weight_decay=HP["wd"], step=2)
+        t_.cuda.synchronize()
+        p1, m1, v1, p16 = oracle.adamw(oracle.aggregate_f32(gs), p, m, v, t=2, **HP)
+        assert_parity({"p": to_host(dp), "m": to_host(dm), "v": to_host(dv), "p16": to_host(d16)},
+                      {"p": p1, "m": m1, "v": v1, "p16": p16}, f"adam_step k={k} n={n}")
+
+
 @pytest.mark.parametrize("want_agg,want_p16", [(False, False), (True, False), (False, True)])
 def test_fused_optional_outputs(want_agg, want_p16):
     for mode in ("fp32", "fixed"):
@@ -494,7 +535,8 @@ def test_quantize_matches_oracle(gdtype, k):
                              outlier_scale=1e6)[0]
         if gdtype == "f32" and n > 8:
             g[:6] = np.array([np.inf, -np.inf, np.nan, 3e38, -3e38, 1e-45], np.float32)
-        for off in ((0, 0), (1, 3)) if n > 4 else ((0, 0),):
+        for off in ((0, 0), (1, 3), (1, 1), (2, 2), (3, 3), (5, 1), (45, 45)) if n > 4 \
+                else ((0, 0), (2, 2), (45, 45)):
             out = to_dev(np.zeros(n, np.int32), off[1])
             dd.quantize(to_dev(g, off[0]), out, frac_bits=k)
             t_.cuda.synchronize()
