@@ -225,7 +225,9 @@ enum {
  *                 relative placement matters: moving a whole layout by
  *                 whole pages streamed at the same rate.
  * Returns DISDP_OK, or DISDP_ERR_INVALID_ARG / DISDP_ERR_UNSUPPORTED for a
- * bad n, W, NULL output or unknown dtype. */
+ * bad n, W, NULL output or unknown dtype, and DISDP_ERR_INVALID_ARG when the
+ * total would not fit in int64 (possible near the largest n with large W);
+ * the outputs may then be partly written. */
 disdp_status_t disdp_shard_layout(int64_t n, int W, disdp_dtype_t gdtype, unsigned flags,
                                   int64_t *offsets, int64_t *total_bytes);
 

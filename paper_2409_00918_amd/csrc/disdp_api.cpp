@@ -367,12 +367,18 @@ disdp_status_t disdp_shard_layout(int64_t n, int W, disdp_dtype_t gdtype, unsign
     int64_t at = 0;          // next free byte, page aligned
     int64_t prev_start = -1;
     int prev_esize = 0;
+    // Every step adds at most 2 pages plus the array: checked against the
+    // int64 range before it is taken (n <= 2^56 and W <= 64 can exceed it).
+    constexpr int64_t kMaxTotal = INT64_MAX;
     for (int i = 0; i < W + 6; ++i) {
         const int esize = esz[i];
         if (esize == 0) {
             offsets[i] = -1;
             continue;
         }
+        const int64_t span = pages(n * esize);
+        if (at > kMaxTotal - 2 * kPage - span)
+            return DISDP_ERR_INVALID_ARG;
         if (prev_start >= 0)
             at += kPage;
         const int64_t page = at / kPage;
@@ -383,7 +389,7 @@ disdp_status_t disdp_shard_layout(int64_t n, int W, disdp_dtype_t gdtype, unsign
         offsets[i] = at;
         prev_start = at;
         prev_esize = esize;
-        at += pages(n * esize);
+        at += span;
     }
     *total_bytes = at;
     return DISDP_OK;

@@ -1,0 +1,427 @@
+// Host-side fuzz of the C-ABI front end (paper_2409_00918_amd/csrc/disdp_api.cpp)
+// built with g++ under AddressSanitizer and UndefinedBehaviorSanitizer,
+// without a GPU: the two HIP runtime calls the front end makes and the two
+// kernel-launch entry points are replaced by the stubs below, which record
+// what would have been launched.
+//
+//   * disdp_shard_layout over random n (up to 2^56), W, dtypes and flags:
+//     status, and every placement invariant of a successful layout;
+//   * each entry point with exactly one argument error injected into an
+//     otherwise valid call: the documented status, and no launch;
+//   * valid calls whose arrays share, or do not share, a misalignment: the
+//     vector/element choice, the head of elements done one by one and the
+//     advanced pointers.
+//
+// Prints "api_fuzz: ok" and exits 0; any failed check prints the case and
+// exits 1; a sanitizer finding aborts.
+#include <cinttypes>
+#include <cmath>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+
+#include "disdp.h"
+#include "disdp_launch.h"
+
+// ---- stubs for what the front end calls below it ---------------------------
+namespace {
+int g_launches = 0;
+int g_queries = 0;
+bool g_addressable = true;
+disdp::LaunchArgs g_args;
+bool g_vec = false;
+disdp::QuantizeArgs g_qargs;
+}  // namespace
+
+namespace disdp {
+hipError_t launch(const LaunchArgs &a, Kind, bool vector_path, hipStream_t)
+{
+    ++g_launches;
+    g_args = a;
+    g_vec = vector_path;
+    return hipSuccess;
+}
+hipError_t launch_quantize(const QuantizeArgs &q, bool vector_path, hipStream_t)
+{
+    ++g_launches;
+    g_qargs = q;
+    g_vec = vector_path;
+    return hipSuccess;
+}
+}  // namespace disdp
+
+extern "C" hipError_t hipPointerGetAttributes(hipPointerAttribute_t *at, const void *p)
+{
+    ++g_queries;
+    std::memset(at, 0, sizeof *at);
+    if (!g_addressable)
+        return hipErrorInvalidValue;
+    at->type = hipMemoryTypeDevice;
+    at->devicePointer = const_cast<void *>(p);
+    return hipSuccess;
+}
+
+extern "C" hipError_t hipGetLastError(void) { return hipSuccess; }
+
+// ---- helpers ------------------------------------------------------------------
+namespace {
+
+uint64_t rng_state = 0x9E3779B97F4A7C15ull;
+uint64_t next()
+{
+    uint64_t x = (rng_state += 0x9E3779B97F4A7C15ull);
+    x = (x ^ (x >> 30)) * 0xBF58476D1CE4E5B9ull;
+    x = (x ^ (x >> 27)) * 0x94D049BB133111EBull;
+    return x ^ (x >> 31);
+}
+int64_t below(int64_t k) { return static_cast<int64_t>(next() % static_cast<uint64_t>(k)); }
+
+int failures = 0;
+#define CHECK(cond, ...)                                                   \
+    do {                                                                   \
+        if (!(cond)) {                                                     \
+            std::printf("FAIL %s:%d: %s: ", __FILE__, __LINE__, #cond);    \
+            std::printf(__VA_ARGS__);                                      \
+            std::printf("\n");                                             \
+            if (++failures > 20)                                           \
+                std::exit(1);                                              \
+        }                                                                  \
+    } while (0)
+
+constexpr int64_t kPage = int64_t(1) << 21;
+
+// ---- disdp_shard_layout --------------------------------------------------------
+void fuzz_layout(int iters)
+{
+    for (int it = 0; it < iters; ++it) {
+        int64_t n;
+        switch (below(6)) {
+        case 0: n = below(5); break;
+        case 1: n = below(1 << 20); break;
+        case 2: n = below(int64_t(1) << 40); break;
+        case 3: n = int64_t(1) << 56; break;
+        case 4: n = below((int64_t(1) << 56) + 1); break;
+        default: n = -below(1000) - 1; break;
+        }
+        const int W = static_cast<int>(below(67));  // 0 and 65, 66 invalid
+        const int gdt = static_cast<int>(below(4));  // 3 invalid
+        const unsigned flags = static_cast<unsigned>(below(8));
+        int64_t off[disdp::kMaxW + 6];
+        int64_t total = -7;
+        const disdp_status_t st =
+            disdp_shard_layout(n, W, static_cast<disdp_dtype_t>(gdt), flags, off, &total);
+        const bool bad_count = n < 0 || n > (int64_t(1) << 56) || W < 1 || W > 64;
+        if (bad_count) {
+            CHECK(st == DISDP_ERR_INVALID_ARG, "n=%" PRId64 " W=%d st=%d", n, W, st);
+            continue;
+        }
+        if (gdt == 3) {
+            CHECK(st == DISDP_ERR_UNSUPPORTED, "gdt=3 st=%d", st);
+            continue;
+        }
+        // element sizes in placement order; 0 = not requested
+        int esz[disdp::kMaxW + 6];
+        for (int w = 0; w < W; ++w)
+            esz[w] = gdt == 1 ? 2 : 4;
+        esz[W] = esz[W + 1] = esz[W + 2] = 4;
+        esz[W + 3] = (flags & 1) ? 2 : 0;
+        esz[W + 4] = (flags & 2) ? 4 : 0;
+        esz[W + 5] = (flags & 4) ? 4 : 0;
+        // a lower bound of the total in 128-bit arithmetic
+        __int128 need = 0;
+        for (int i = 0; i < W + 6; ++i)
+            if (esz[i])
+                need += (static_cast<__int128>(n) * esz[i] + kPage - 1) / kPage * kPage;
+        if (st != DISDP_OK) {
+            CHECK(st == DISDP_ERR_INVALID_ARG && need > (static_cast<__int128>(INT64_MAX) / 2),
+                  "refused a layout of %.3g bytes: st=%d", static_cast<double>(need), st);
+            continue;
+        }
+        CHECK(need <= INT64_MAX, "accepted an int64-overflowing layout");
+        int64_t prev_end = -1, prev_start = -1;
+        int prev_esize = 0;
+        for (int i = 0; i < W + 6; ++i) {
+            if (!esz[i]) {
+                CHECK(off[i] == -1, "array %d not requested but placed", i);
+                continue;
+            }
+            CHECK(off[i] >= 0 && off[i] % kPage == 0, "array %d offset %" PRId64, i, off[i]);
+            if (prev_end >= 0)
+                CHECK(off[i] >= prev_end + kPage, "array %d closer than a page", i);
+            if (esz[i] == 4)
+                CHECK((off[i] / kPage) % 2 == 0, "4-byte array %d on an odd page", i);
+            if (esz[i] == 2 && prev_esize == 2)
+                CHECK(((off[i] - prev_start) / kPage) % 2 == 1,
+                      "2-byte array %d an even number of pages after the previous", i);
+            const int64_t end = off[i] + n * esz[i];
+            CHECK(end <= total, "array %d ends past the total", i);
+            prev_end = end;
+            prev_start = off[i];
+            prev_esize = esz[i];
+        }
+    }
+}
+
+// ---- one error injected into a valid call ---------------------------------------
+struct Call {
+    int entry;  // 0 aggregate, 1 adam_step, 2 aggregate_adam, 3 quantize
+    int W, gdt, mode, k;
+    int64_t n;
+    const void *g[disdp::kMaxW];
+    const void *const *grads;
+    float *p, *m, *v, *af;
+    uint16_t *p16;
+    int32_t *ai;
+    disdp_adamw_hparams_t hp;
+    bool hp_null;
+};
+
+// Fake, never dereferenced, well separated addresses: array i at base + i * 2^40.
+char *fake(int i) { return reinterpret_cast<char *>((uintptr_t(1) << 44) + (uintptr_t(i) << 40)); }
+
+Call valid_call(int entry)
+{
+    Call c{};
+    c.entry = entry;
+    c.W = entry == 1 || entry == 3 ? 1 : 1 + static_cast<int>(below(64));
+    c.mode = entry == 1 ? DISDP_AGG_FP32 : static_cast<int>(below(2));
+    c.gdt = entry == 1 ? DISDP_DT_F32
+            : (c.mode == DISDP_AGG_FIXED && entry != 3) ? static_cast<int>(below(3))
+                                                        : static_cast<int>(below(2));
+    c.k = static_cast<int>(below(31));
+    c.n = 1 + below(1 << 30);
+    for (int w = 0; w < c.W; ++w)
+        c.g[w] = fake(w);
+    c.grads = c.g;
+    c.p = reinterpret_cast<float *>(fake(70));
+    c.m = reinterpret_cast<float *>(fake(71));
+    c.v = reinterpret_cast<float *>(fake(72));
+    c.p16 = below(2) ? reinterpret_cast<uint16_t *>(fake(73)) : nullptr;
+    c.af = reinterpret_cast<float *>(fake(74));
+    c.ai = c.mode == DISDP_AGG_FIXED ? reinterpret_cast<int32_t *>(fake(75)) : nullptr;
+    if (entry == 2 && below(2)) {
+        c.af = nullptr;
+        c.ai = nullptr;
+    }
+    c.hp = {1e-4f, 0.9f, 0.95f, 1e-8f, 0.1f, 1 + below(100000), 1.0f};
+    return c;
+}
+
+disdp_status_t issue(const Call &c)
+{
+    const disdp_adamw_hparams_t *hp = c.hp_null ? nullptr : &c.hp;
+    switch (c.entry) {
+    case 0:
+        return disdp_aggregate(c.grads, c.W, static_cast<disdp_dtype_t>(c.gdt), c.n,
+                               static_cast<disdp_agg_mode_t>(c.mode), c.k, c.af, c.ai, nullptr);
+    case 1:
+        return disdp_adam_step(c.grads ? static_cast<const float *>(c.grads[0]) : nullptr, c.p,
+                               c.m, c.v, c.p16, c.n, hp, nullptr);
+    case 2:
+        return disdp_aggregate_adam(c.grads, c.W, static_cast<disdp_dtype_t>(c.gdt), c.n,
+                                    static_cast<disdp_agg_mode_t>(c.mode), c.k, c.p, c.m, c.v,
+                                    c.p16, c.af, c.ai, hp, nullptr);
+    default:
+        return disdp_quantize(c.grads ? c.grads[0] : nullptr,
+                              static_cast<disdp_dtype_t>(c.gdt), c.n, c.k,
+                              c.ai ? c.ai : reinterpret_cast<int32_t *>(fake(75)), nullptr);
+    }
+}
+
+void fuzz_errors(int iters)
+{
+    for (int it = 0; it < iters; ++it) {
+        const int entry = static_cast<int>(below(4));
+        Call c = valid_call(entry);
+        if (entry == 0 && c.mode == DISDP_AGG_FP32 && !c.af)
+            c.af = reinterpret_cast<float *>(fake(74));
+        if (entry == 0 && c.mode == DISDP_AGG_FIXED && !c.af && !c.ai)
+            c.ai = reinterpret_cast<int32_t *>(fake(75));
+        disdp_status_t want = DISDP_OK;
+        const int kind = static_cast<int>(below(12));
+        switch (kind) {
+        case 0:  // n out of range
+            c.n = below(2) ? -1 - below(100) : (int64_t(1) << 56) + 1 + below(100);
+            want = DISDP_ERR_INVALID_ARG;
+            break;
+        case 1:  // W out of range (the two single-buffer calls have none)
+            if (entry == 0 || entry == 2) {
+                c.W = below(2) ? 0 : 65 + static_cast<int>(below(100));
+                want = DISDP_ERR_INVALID_ARG;
+            }
+            break;
+        case 2:  // unknown dtype or mode
+            if (entry != 1) {
+                if (below(2) || entry == 3)
+                    c.gdt = 3 + static_cast<int>(below(5));
+                else
+                    c.mode = 2 + static_cast<int>(below(5));
+                want = DISDP_ERR_UNSUPPORTED;
+            }
+            break;
+        case 3:  // bad frac_bits in fixed mode (quantize: always checked)
+            if ((entry != 1 && c.mode == DISDP_AGG_FIXED) || entry == 3) {
+                c.k = below(2) ? -1 - static_cast<int>(below(10)) : 31 + static_cast<int>(below(10));
+                want = DISDP_ERR_INVALID_ARG;
+            }
+            break;
+        case 4:  // bad hyperparameters
+            if (entry == 1 || entry == 2) {
+                switch (below(7)) {
+                case 0: c.hp.step = -below(5); break;
+                case 1: c.hp.beta1 = 1.0f; break;
+                case 2: c.hp.beta2 = NAN; break;
+                case 3: c.hp.eps = -1e-8f; break;
+                case 4: c.hp.lr = INFINITY; break;
+                case 5: c.hp.grad_scale = NAN; break;
+                default: c.hp_null = true; break;
+                }
+                want = DISDP_ERR_INVALID_ARG;
+            }
+            break;
+        case 5:  // NULL contribution array or pointer
+            if (below(2) && entry != 1 && entry != 3)
+                c.grads = nullptr;
+            else
+                c.g[below(c.W)] = nullptr;
+            want = DISDP_ERR_INVALID_ARG;
+            break;
+        case 6:  // NULL state
+            if (entry == 1 || entry == 2) {
+                c.m = nullptr;
+                want = DISDP_ERR_INVALID_ARG;
+            }
+            break;
+        case 7:  // an output overlapping a contribution somewhere inside it
+            if (entry == 0 && c.af) {
+                c.af = reinterpret_cast<float *>(const_cast<char *>(
+                    static_cast<const char *>(c.g[below(c.W)]) +
+                    (c.gdt == DISDP_DT_BF16 ? 2 : 4) * below(c.n)));
+                want = DISDP_ERR_ALIAS;
+            } else if (entry == 1 || entry == 2) {
+                c.v = reinterpret_cast<float *>(const_cast<char *>(
+                    static_cast<const char *>(c.g[below(c.W)]) + 2 * below(c.n)));
+                want = DISDP_ERR_ALIAS;
+            } else if (entry == 3) {
+                c.ai = reinterpret_cast<int32_t *>(const_cast<char *>(
+                    static_cast<const char *>(c.g[0]) + 2 * below(c.n)));
+                want = DISDP_ERR_ALIAS;
+            }
+            break;
+        case 8:  // two outputs overlapping
+            if (entry == 1 || entry == 2) {
+                c.p = c.m + below(c.n);
+                want = DISDP_ERR_ALIAS;
+            }
+            break;
+        case 9:  // an int32 aggregate in fp32 mode
+            if ((entry == 0 || entry == 2) && c.mode == DISDP_AGG_FP32) {
+                c.ai = reinterpret_cast<int32_t *>(fake(75));
+                want = DISDP_ERR_INVALID_ARG;
+            }
+            break;
+        case 10:  // memory the GPU cannot address
+            g_addressable = false;
+            want = DISDP_ERR_INVALID_ARG;
+            break;
+        default:  // empty shard: accepted, nothing launched
+            c.n = 0;
+            c.grads = below(2) ? nullptr : c.grads;
+            want = DISDP_OK;
+            break;
+        }
+        const int launches = g_launches;
+        const disdp_status_t st = issue(c);
+        g_addressable = true;
+        CHECK(st == want, "entry %d kind %d: status %d, want %d (W=%d gdt=%d mode=%d n=%" PRId64
+              ")", entry, kind, st, want, c.W, c.gdt, c.mode, c.n);
+        const bool launched = g_launches != launches;
+        CHECK(launched == (want == DISDP_OK && c.n > 0),
+              "entry %d kind %d: launched=%d", entry, kind, launched);
+        CHECK(std::strlen(disdp_status_string(st)) > 0, "empty status string");
+    }
+    for (int s = -5; s < 10; ++s)
+        CHECK(disdp_status_string(static_cast<disdp_status_t>(s)) != nullptr, "status %d", s);
+}
+
+// ---- valid calls: which kernel, head and advanced pointers ------------------------
+void fuzz_alignment(int iters)
+{
+    for (int it = 0; it < iters; ++it) {
+        const int W = 1 + static_cast<int>(below(16));
+        const int gdt = static_cast<int>(below(2));
+        const int gb = gdt == 1 ? 2 : 4;
+        const int64_t n = 1 + (below(2) ? below(130) : below(1 << 24));
+        // every array on a 1 KiB boundary plus a shared phase, then optionally
+        // disturbed: a different phase mod 64 but the same mod 4, a different
+        // phase mod 4, or an address not a multiple of the element size
+        const int phase = static_cast<int>(below(64));
+        const int disturb = static_cast<int>(below(4));
+        const int victim = static_cast<int>(below(W + 4));
+        int extra = 0;
+        if (disturb == 1)
+            extra = 4 * (1 + static_cast<int>(below(15)));
+        else if (disturb == 2)
+            extra = 1 + static_cast<int>(below(3));
+        const void *g[disdp::kMaxW];
+        for (int w = 0; w < W; ++w)
+            g[w] = fake(w) + int64_t(gb) * (phase + (victim == w ? extra : 0)) +
+                   (disturb == 3 && victim == w ? 1 : 0);
+        auto arr = [&](int idx, int esz) {
+            return fake(70 + idx) + int64_t(esz) * (phase + (victim == W + idx ? extra : 0)) +
+                   (disturb == 3 && victim == W + idx ? 1 : 0);
+        };
+        float *p = reinterpret_cast<float *>(arr(0, 4));
+        float *m = reinterpret_cast<float *>(arr(1, 4));
+        float *v = reinterpret_cast<float *>(arr(2, 4));
+        uint16_t *p16 = reinterpret_cast<uint16_t *>(arr(3, 2));
+        const disdp_adamw_hparams_t hp = {1e-4f, 0.9f, 0.95f, 1e-8f, 0.1f, 3, 1.0f};
+        const disdp_status_t st = disdp_aggregate_adam(g, W, static_cast<disdp_dtype_t>(gdt), n,
+                                                       DISDP_AGG_FP32, 0, p, m, v, p16, nullptr,
+                                                       nullptr, &hp, nullptr);
+        CHECK(st == DISDP_OK, "status %d", st);
+        const disdp::LaunchArgs &a = g_args;
+        // disturb 0: one shared phase mod 64 -> head to the 64-element
+        // boundary; 1: same phase mod 4 only -> head to the 4-element one;
+        // 2, 3: no shared phase or a misaligned element -> element kernel
+        bool want_vec = disturb <= 1;
+        int64_t want_head = disturb == 0 ? (64 - phase) & 63 : disturb == 1 ? (4 - (phase & 3)) & 3 : 0;
+        if (want_head > n)
+            want_head = n;
+        CHECK(g_vec == want_vec, "vec %d want %d (disturb %d phase %d)", g_vec, want_vec, disturb,
+              phase);
+        CHECK(a.head == want_head, "head %d want %d (disturb %d phase %d n %" PRId64 ")", a.head,
+              static_cast<int>(want_head), disturb, phase, n);
+        CHECK(a.head + a.n == n, "head %d + n %" PRId64 " != %" PRId64, a.head, a.n, n);
+        CHECK(a.p == p + a.head && a.m == m + a.head && a.v == v + a.head &&
+                  a.p16 == p16 + a.head,
+              "state pointers not advanced by the head");
+        for (int w = 0; w < W; ++w)
+            CHECK(a.g[w] == static_cast<const char *>(g[w]) + int64_t(a.head) * gb,
+                  "contribution %d not advanced by the head", w);
+        if (g_vec && a.n > 0) {
+            const int gran = disturb == 0 ? 64 : 4;
+            for (int w = 0; w < W; ++w)
+                CHECK((reinterpret_cast<uintptr_t>(a.g[w]) / gb) % gran == 0,
+                      "contribution %d not on a %d-element boundary", w, gran);
+            CHECK((reinterpret_cast<uintptr_t>(a.p) / 4) % gran == 0 &&
+                      (reinterpret_cast<uintptr_t>(a.p16) / 2) % gran == 0,
+                  "state not on a %d-element boundary", gran);
+        }
+    }
+}
+
+}  // namespace
+
+int main()
+{
+    fuzz_layout(200000);
+    fuzz_errors(200000);
+    fuzz_alignment(100000);
+    if (failures) {
+        std::printf("api_fuzz: %d failures\n", failures);
+        return 1;
+    }
+    std::printf("api_fuzz: ok\n");
+    return 0;
+}

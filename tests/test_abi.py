@@ -347,3 +347,14 @@ def test_binding_refuses_a_call_spanning_two_gpus():
     assert dd._device([host, None]) is None
     with pytest.raises(ValueError, match="one GPU"):
         dd._device([g0, host, g1])
+
+
+def test_shard_layout_refuses_a_total_beyond_int64():
+    """n may be as large as 2^56, but with many contributions the layout's
+    total would not fit in int64: refused rather than wrapped."""
+    import paper_2409_00918_amd as dd
+    with pytest.raises(dd.DisdpError) as ei:
+        dd.shard_layout(1 << 56, 64, "f32")
+    assert ei.value.status == dd.ERR_INVALID_ARG
+    offs, total = dd.shard_layout(1 << 56, 1, "bf16")
+    assert 0 < total < 2 ** 63 and offs[1] >= (1 << 57)

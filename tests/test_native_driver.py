@@ -13,6 +13,7 @@ import oracle
 HERE = os.path.dirname(os.path.abspath(__file__))
 EXE = os.path.join(HERE, "native", "abi_driver")
 PKG_LIB = os.path.join(os.path.dirname(HERE), "paper_2409_00918_amd", "libdisdp.so")
+FUZZ = os.path.join(HERE, "native", "api_fuzz")
 
 
 def _exe():
@@ -39,3 +40,15 @@ def test_c_abi_from_a_plain_cpp_program_matches_the_oracle():
     print(r.stderr)
     assert r.returncode == 0, r.stdout + r.stderr
     assert "abi_driver: all ok" in r.stdout
+
+
+def test_api_front_end_fuzz_under_sanitizers():
+    """CPU: the front end's argument checks, the layout planner and the
+    choice of kernel, head and advanced pointers, over 500,000 random calls
+    with AddressSanitizer and UndefinedBehaviorSanitizer (any finding
+    aborts)."""
+    if not os.path.exists(FUZZ):
+        pytest.fail(f"{FUZZ} is not built (python tests/native/build.py)")
+    r = subprocess.run([FUZZ], capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0, r.stdout[-3000:] + r.stderr[-3000:]
+    assert "api_fuzz: ok" in r.stdout
