@@ -32,12 +32,15 @@
 // One rounding per written operation: never contract a*b+c into an FMA.
 #pragma clang fp contract(off)
 
-// Launch-shape tunables (compile-time).  The defaults -- one 256-lane tile
-// per block, one group per lane, non-temporal loads and stores, tiles in
-// natural order -- were the best or tied-best in interleaved A/B runs on
-// MI355X over the 7B/8, 13B/16 and 175B/64 shards; the other settings were
-// within 2% or slower (persistent grids, more groups per lane, wider blocks,
-// wave-contiguous groups, XCD-chunked tile orders, hints on one side only).
+// Launch-shape tunables (compile-time).  The defaults -- one-wave (64-lane)
+// blocks each owning one tile, one group per lane, non-temporal loads and
+// stores, tiles in natural order -- were the best or tied-best in
+// interleaved A/B runs on MI355X over the 7B/8, 13B/16 and 175B/64 shards;
+// the other settings were within 2% or slower (persistent grids, more
+// groups per lane, 128- to 1024-lane blocks, wave-contiguous groups,
+// XCD-chunked tile orders, hints on one side only).  One-wave blocks beat
+// 256-lane blocks at the same resident waves by 2-6%: a retiring wave frees
+// its slot at once instead of waiting for the slowest wave of its block.
 //   DISDP_UNROLL      groups of 4 elements per lane per tile (loads in flight)
 //   DISDP_GRID_MODE   0: persistent grid of (resident blocks per CU) x CUs x
 //                        DISDP_GRID_ROUNDS blocks, tiles grid-stride;
@@ -47,25 +50,23 @@
 //   DISDP_WAVE_CONTIG 1: a wave's U groups are contiguous (U KiB per fp32
 //                     stream per wave); 0: strided by the block width
 //   DISDP_MIN_WAVES   launch-bounds hint: waves per SIMD to fit (0 = none)
-//   DISDP_BLOCKS_PER_CU  resident blocks per CU for the fp32-mode fused and
+//   DISDP_WAVES_PER_CU  resident waves per CU for the fp32-mode fused and
 //                     aggregation vector kernels (0 = as many as registers
-//                     allow).  Enforced by reserving 1/k of the CU's LDS per
-//                     block (the kernels use no LDS).  With W + 3 16-byte
-//                     loads in flight per lane, 2-3 blocks (8-12 waves,
-//                     ~135 KB in flight per CU) stream fastest: more
-//                     outstanding requests cost DRAM efficiency, 1 block is
-//                     too few.
-//   DISDP_BLOCKS_PER_CU_SMALL  the cap for fp32-mode kernels whose lanes keep
+//                     allow), enforced in whole blocks by reserving a share
+//                     of the CU's LDS per block (the kernels use no LDS).
+//                     With W + 3 16-byte loads in flight per lane, 8-12
+//                     waves (~135 KB in flight per CU) stream fastest: more
+//                     outstanding requests cost DRAM efficiency, 4 are too
+//                     few.
+//   DISDP_WAVES_PER_CU_SMALL  the cap for fp32-mode kernels whose lanes keep
 //                     at most DISDP_SMALL_LANE_BYTES of loads in flight
 //                     (W <= 2 fp32 contributions with the optimizer, the
-//                     optimizer step alone): fewer bytes per wave need one
-//                     more block per CU (+1.5 to +3% at cap 4; W = 4 and
-//                     larger are best at 3).
-//   DISDP_BLOCKS_PER_CU_FIXED  the same for fixed-point mode, whose lanes
+//                     optimizer step alone): fewer bytes per wave need more
+//                     waves.
+//   DISDP_WAVES_PER_CU_FIXED  the same for fixed-point mode, whose lanes
 //                     spend ~4x more instructions per element converting
 //                     contributions and so need more resident waves to keep
-//                     loads in flight: 5 blocks (the aggregation +7%, the
-//                     fused call +2% over 3).
+//                     loads in flight.
 //                     The quantize kernel (one load per lane) is not capped.
 //   DISDP_XCD_CHUNK   0: block b takes tile b.  C > 0 (one tile per block):
 //                     the dispatcher deals blocks round-robin to the 8
@@ -86,7 +87,10 @@
 #define DISDP_NT 3
 #endif
 #ifndef DISDP_BLOCK
-#define DISDP_BLOCK 256
+#define DISDP_BLOCK 64
+#endif
+#ifndef DISDP_QUANT_BLOCK
+#define DISDP_QUANT_BLOCK 64  // lanes per block of the quantize kernels
 #endif
 #ifndef DISDP_WAVE_CONTIG
 #define DISDP_WAVE_CONTIG 0
@@ -94,14 +98,14 @@
 #ifndef DISDP_MIN_WAVES
 #define DISDP_MIN_WAVES 0
 #endif
-#ifndef DISDP_BLOCKS_PER_CU
-#define DISDP_BLOCKS_PER_CU 3
+#ifndef DISDP_WAVES_PER_CU
+#define DISDP_WAVES_PER_CU 8
 #endif
-#ifndef DISDP_BLOCKS_PER_CU_FIXED
-#define DISDP_BLOCKS_PER_CU_FIXED 5
+#ifndef DISDP_WAVES_PER_CU_FIXED
+#define DISDP_WAVES_PER_CU_FIXED 12
 #endif
-#ifndef DISDP_BLOCKS_PER_CU_SMALL
-#define DISDP_BLOCKS_PER_CU_SMALL 4
+#ifndef DISDP_WAVES_PER_CU_SMALL
+#define DISDP_WAVES_PER_CU_SMALL 12
 #endif
 #ifndef DISDP_SMALL_LANE_BYTES
 #define DISDP_SMALL_LANE_BYTES 80
@@ -118,12 +122,17 @@ constexpr int kXcds = 8;
 #else
 #define DISDP_LAUNCH_BOUNDS __launch_bounds__(DISDP_BLOCK)
 #endif
+#define DISDP_QUANT_LAUNCH_BOUNDS __launch_bounds__(DISDP_QUANT_BLOCK)
 
 namespace disdp {
 namespace {
 
 constexpr int kBlock = DISDP_BLOCK;
-[[maybe_unused]] constexpr int kWave = 64;  // used by DISDP_WAVE_CONTIG
+constexpr int kQuantBlock = DISDP_QUANT_BLOCK;
+// block 0 does up to 63 head elements and 3 tail elements, one per lane
+static_assert(DISDP_BLOCK % 64 == 0 && DISDP_QUANT_BLOCK % 64 == 0,
+              "blocks are whole 64-lane waves");
+constexpr int kWave = 64;
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
@@ -507,14 +516,15 @@ __global__ DISDP_LAUNCH_BOUNDS void element_kernel(LaunchArgs a)
 
 // ---- the format conversion as a producer ------------------------------------
 
-// out = quantize(g) over 4-element groups (one group per lane, one
-// 256-lane tile per block), the last n % 4 elements by block 0.
+// out = quantize(g) over 4-element groups (one group per lane, grid-stride
+// over kQuantBlock-lane blocks), the last n % 4 and the head elements by
+// block 0.
 template <int GT>
-__global__ DISDP_LAUNCH_BOUNDS void quantize_vector_kernel(QuantizeArgs q)
+__global__ DISDP_QUANT_LAUNCH_BOUNDS void quantize_vector_kernel(QuantizeArgs q)
 {
     const int64_t n_groups = q.n >> 2;
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
-    for (int64_t grp = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; grp < n_groups;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kQuantBlock;
+    for (int64_t grp = static_cast<int64_t>(blockIdx.x) * kQuantBlock + threadIdx.x; grp < n_groups;
          grp += stride) {
         float x[4];
         load_group<GT>(q.g, grp, x);
@@ -533,10 +543,10 @@ __global__ DISDP_LAUNCH_BOUNDS void quantize_vector_kernel(QuantizeArgs q)
 }
 
 template <int GT>
-__global__ DISDP_LAUNCH_BOUNDS void quantize_element_kernel(QuantizeArgs q)
+__global__ DISDP_QUANT_LAUNCH_BOUNDS void quantize_element_kernel(QuantizeArgs q)
 {
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
-    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < q.n; i += stride)
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kQuantBlock;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kQuantBlock + threadIdx.x; i < q.n; i += stride)
         q.out[i] = quantize(load_one<GT>(q.g, i), q.qscale);
 }
 
@@ -548,7 +558,7 @@ constexpr int kU = DISDP_UNROLL;
 // `blocks_per_cu` blocks fit on a CU (0 = no cap), cached per device.
 int occupancy_lds_bytes(int blocks_per_cu)
 {
-    constexpr int kMaxCap = 16;
+    constexpr int kMaxCap = 64;
     if (blocks_per_cu <= 0 || blocks_per_cu > kMaxCap)
         return 0;
     static std::atomic<int> cached[64][kMaxCap + 1];
@@ -611,23 +621,32 @@ int stream_cus(hipStream_t stream)
     return c > 0 ? c : total;
 }
 
-// Resident-block cap per CU for a launch on `stream`: `base` is the cap for
-// the whole chip.  What streams best is a number of resident blocks
-// chip-wide, so on a stream restricted to fewer CUs each CU takes
-// proportionally more, up to kMaxScaledCap (the register limit of the
-// W = 8 kernels).  Measured on the 7B/8 shard with 32 / 64 / 128 CUs: cap 5
-// streamed 41% / 35% / 19% faster than cap 3, which is best on all 256.
-constexpr int kMaxScaledCap = 5;
-int blocks_per_cu_cap(int base, hipStream_t stream)
+// Resident-block cap per CU for a launch on `stream`: `base_waves` is the
+// cap in waves for the whole chip.  What streams best is a number of
+// resident waves chip-wide, so on a stream restricted to fewer CUs each CU
+// takes proportionally more, up to kMaxScaledWaves (the register limit of
+// the W = 8 kernels).  Measured on the 7B/8 shard with 32 / 64 / 128 CUs:
+// 20 waves per CU streamed 41% / 35% / 19% faster than 12, which is best
+// on all 256.
+#ifndef DISDP_MAX_SCALED_WAVES
+#define DISDP_MAX_SCALED_WAVES 20
+#endif
+constexpr int kMaxScaledWaves = DISDP_MAX_SCALED_WAVES;
+int blocks_per_cu_cap(int base_waves, hipStream_t stream)
 {
-    if (base <= 0)
+    if (base_waves <= 0)
         return 0;
     const int total = cu_count();
     const int mine = stream_cus(stream);
-    if (mine >= total)
-        return base;
-    const int scaled = (base * total + mine - 1) / mine;
-    return scaled < kMaxScaledCap ? scaled : (base > kMaxScaledCap ? base : kMaxScaledCap);
+    int waves = base_waves;
+    if (mine < total) {
+        const int scaled = (base_waves * total + mine - 1) / mine;
+        waves = scaled < kMaxScaledWaves ? scaled
+                                         : (base_waves > kMaxScaledWaves ? base_waves : kMaxScaledWaves);
+    }
+    constexpr int kWavesPerBlock = kBlock / kWave;
+    const int blocks = waves / kWavesPerBlock;
+    return blocks > 0 ? blocks : 1;
 }
 
 // Blocks of `fn` that fit on one CU at once (registers, or the reserved
@@ -701,9 +720,9 @@ hipError_t launch_vector(const LaunchArgs &a, hipStream_t stream)
     // contribution, plus p, m and v with the optimizer
     constexpr int kGradBytes = GT == kGradBF16 ? 2 : 4;
     constexpr int kLaneBytes = W > 0 ? 4 * (W * kGradBytes + (ADAM ? 12 : 0)) : 1 << 30;
-    constexpr int base = MODE == kAggFixed ? DISDP_BLOCKS_PER_CU_FIXED
-                         : kLaneBytes <= DISDP_SMALL_LANE_BYTES ? DISDP_BLOCKS_PER_CU_SMALL
-                                                                : DISDP_BLOCKS_PER_CU;
+    constexpr int base = MODE == kAggFixed ? DISDP_WAVES_PER_CU_FIXED
+                         : kLaneBytes <= DISDP_SMALL_LANE_BYTES ? DISDP_WAVES_PER_CU_SMALL
+                                                                : DISDP_WAVES_PER_CU;
     return launch_kernel(reinterpret_cast<const void *>(&vector_kernel<W, GT, MODE, ADAM, U>),
                          blocks, DISDP_GRID_MODE == 0, a, stream,
                          occupancy_lds_bytes(blocks_per_cu_cap(base, stream)));
@@ -757,18 +776,19 @@ hipError_t launch_quantize(const QuantizeArgs &q, bool vector_path, hipStream_t 
     if (vector_path) {
         fn = q.gdtype == kGradBF16 ? reinterpret_cast<const void *>(&quantize_vector_kernel<kGradBF16>)
                                    : reinterpret_cast<const void *>(&quantize_vector_kernel<kGradF32>);
-        blocks = ceil_div(q.n >> 2, kBlock);
+        blocks = ceil_div(q.n >> 2, kQuantBlock);
     } else {
         fn = q.gdtype == kGradBF16 ? reinterpret_cast<const void *>(&quantize_element_kernel<kGradBF16>)
                                    : reinterpret_cast<const void *>(&quantize_element_kernel<kGradF32>);
-        blocks = ceil_div(q.n, kBlock);
+        blocks = ceil_div(q.n, kQuantBlock);
     }
     if (blocks > 0x7fffffff)
         blocks = 0x7fffffff;   // the kernels are grid-stride
     if (blocks < 1)
         blocks = 1;
     void *args[] = {const_cast<QuantizeArgs *>(&q)};
-    return hipLaunchKernel(fn, dim3(static_cast<unsigned>(blocks)), dim3(kBlock), args, 0, stream);
+    return hipLaunchKernel(fn, dim3(static_cast<unsigned>(blocks)), dim3(kQuantBlock), args, 0,
+                           stream);
 }
 
 }  // namespace disdp
