@@ -22,7 +22,7 @@ from gpu_common import assert_parity, to_host, torch
 pytestmark = pytest.mark.gpu
 
 SAMPLE = 1 << 18
-TILE = 1024            # elements per block tile in the vector kernels (256 lanes x 4)
+TILE = 256             # elements per block tile in the vector kernels (64 lanes x 4)
 
 
 def sample_indices(n, seed):

@@ -19,10 +19,11 @@ from gpu_common import (HP, assert_parity, bits, f32_same, run_fused_case,
 pytestmark = pytest.mark.gpu
 
 # lengths: empty-ish, below one vector group, around 4-element groups,
-# around one wave / block / tile (256 lanes, 2 groups per lane), and larger
-# ragged shards spanning many tiles
-LENGTHS = [1, 2, 3, 4, 5, 7, 8, 9, 63, 255, 256, 257, 1023, 1024, 1025, 2047,
-           2048, 2049, 2051, 4099, 65541, 300_007]
+# around one tile (a one-wave block: 64 lanes x 4 elements = 256) and a few
+# tiles, around 256-lane tiles (1024), and larger ragged shards spanning
+# many tiles
+LENGTHS = [1, 2, 3, 4, 5, 7, 8, 9, 63, 255, 256, 257, 511, 513, 1023, 1024, 1025,
+           2047, 2048, 2049, 2051, 4099, 65541, 300_007]
 
 
 @pytest.fixture(scope="module", autouse=True)
