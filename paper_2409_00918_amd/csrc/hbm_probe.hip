@@ -1,16 +1,19 @@
 // Measurement helper for the benchmark, not part of the libdisdp ABI: a
 // plain device-to-device copy of known size, written the way the fused
-// kernels stream memory (16-byte non-temporal loads and stores, one
-// 256-lane tile per block).  It gives the HBM bandwidth a simple copy reaches
-// on the GPU at hand, and the known byte count against which rocprofv3's
-// FETCH_SIZE / WRITE_SIZE counters are scaled.
+// kernels stream memory (16-byte non-temporal loads and stores, one-wave
+// blocks).  It gives the HBM bandwidth a simple copy reaches on the GPU at
+// hand, and the known byte count against which rocprofv3's FETCH_SIZE /
+// WRITE_SIZE counters are scaled.  Of the copies tried on MI355X (64- or
+// 256-lane blocks, one or two 16-byte vectors per lane, occupancy caps of
+// 8-24 waves per CU) this one was fastest: 6.70 TB/s against 6.45 with
+// 256-lane blocks; every cap made it slower.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
 
 namespace {
 
-constexpr int kBlock = 256;
+constexpr int kBlock = 64;
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 __global__ __launch_bounds__(kBlock) void copy16(const f32x4 *__restrict__ src,
@@ -24,7 +27,7 @@ __global__ __launch_bounds__(kBlock) void copy16(const f32x4 *__restrict__ src,
 }  // namespace
 
 // Copies `bytes` bytes (a multiple of 16, both pointers 16-byte aligned,
-// regions not overlapping, bytes / 16 < 2^31 * 256) from src to dst on
+// regions not overlapping, bytes / 16 < 2^31 * 64) from src to dst on
 // `stream`.  Returns 0, or -1 for bad arguments (nothing launched), or the
 // HIP error code of the launch.
 extern "C" int disdp_probe_copy(const void *src, void *dst, int64_t bytes, hipStream_t stream)
