@@ -186,27 +186,52 @@ def _dev_ptr(t, name: str, n: int, dtypes) -> int:
     return t.data_ptr()
 
 
-def _device(tensors):
-    """The one GPU the device tensors among `tensors` live on (None when all
-    are pinned host memory); a call never spans devices."""
-    devs = {t.device for t in tensors if t is not None and t.is_cuda}
-    if len(devs) > 1:
-        raise ValueError("all device tensors of one call must be on one GPU, got "
-                         + ", ".join(sorted(str(d) for d in devs)))
-    return devs.pop() if devs else None
+def _device_index(tensors) -> int:
+    """Index of the one GPU the device tensors among `tensors` live on (-1
+    when all are pinned host memory); a call never spans devices."""
+    idx = -1
+    for t in tensors:
+        if t is None:
+            continue
+        d = t.get_device()           # -1 for host tensors
+        if d < 0:
+            continue
+        if idx < 0:
+            idx = d
+        elif d != idx:
+            raise ValueError(f"all device tensors of one call must be on one GPU, got "
+                             f"cuda:{idx} and cuda:{d}")
+    return idx
+
+
+_raw_stream = None
+
+
+def _current_stream_handle(idx: int) -> int:
+    """torch's current HIP stream of device `idx`, as a raw handle (the
+    C-level query when this torch has it: the public one builds a Stream
+    object per call)."""
+    global _raw_stream
+    if _raw_stream is None:
+        torch = _torch()
+        _raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None) or \
+            (lambda i: torch.cuda.current_stream(i).cuda_stream)
+    return _raw_stream(idx)
 
 
 def _launch(fn, tensors, stream, *args):
-    """Call `fn(*args, hip_stream)` with that GPU current: the library
-    launches on the current device.  The stream is the one given, else
-    torch's current stream of that device."""
+    """Call `fn(*args, hip_stream)` with the tensors' GPU current: the
+    library launches on the current device.  The stream is the one given,
+    else torch's current stream of that device."""
     torch = _torch()
-    dev = _device(tensors)
-    with torch.cuda.device(dev if dev is not None else torch.cuda.current_device()):
-        if stream is None:
-            s = torch.cuda.current_stream().cuda_stream
-        else:
-            s = getattr(stream, "cuda_stream", stream)
+    idx = _device_index(tensors)
+    cur = torch.cuda.current_device()
+    if idx < 0:
+        idx = cur
+    s = _current_stream_handle(idx) if stream is None else getattr(stream, "cuda_stream", stream)
+    if idx == cur:
+        return fn(*args, s)
+    with torch.cuda.device(idx):
         return fn(*args, s)
 
 

@@ -138,27 +138,30 @@ void fuzz_layout(int iters)
             continue;
         }
         CHECK(need <= INT64_MAX, "accepted an int64-overflowing layout");
-        int64_t prev_end = -1, prev_start = -1;
-        int prev_esize = 0;
+        if (n == 0) {
+            CHECK(total == 0, "n = 0: total %" PRId64, total);
+            for (int i = 0; i < W + 6; ++i)
+                CHECK(off[i] == (esz[i] ? 0 : -1), "n = 0: array %d at %" PRId64, i, off[i]);
+            continue;
+        }
+        const int64_t kAlign = 16 * kPage, kGap = 17 * kPage;
+        int64_t prev_end = -1;
         for (int i = 0; i < W + 6; ++i) {
             if (!esz[i]) {
                 CHECK(off[i] == -1, "array %d not requested but placed", i);
                 continue;
             }
-            CHECK(off[i] >= 0 && off[i] % kPage == 0, "array %d offset %" PRId64, i, off[i]);
-            if (prev_end >= 0)
-                CHECK(off[i] >= prev_end + kPage, "array %d closer than a page", i);
-            if (esz[i] == 4)
-                CHECK((off[i] / kPage) % 2 == 0, "4-byte array %d on an odd page", i);
-            if (esz[i] == 2 && prev_esize == 2)
-                CHECK(((off[i] - prev_start) / kPage) % 2 == 1,
-                      "2-byte array %d an even number of pages after the previous", i);
-            const int64_t end = off[i] + n * esz[i];
+            CHECK(off[i] >= 0 && off[i] % kAlign == 0, "array %d offset %" PRId64, i, off[i]);
+            if (prev_end < 0)
+                CHECK(off[i] == 0, "first array at %" PRId64, off[i]);
+            else
+                CHECK(off[i] >= prev_end + kGap && off[i] - kAlign < prev_end + kGap,
+                      "array %d not at the first boundary 17 pages past the previous end", i);
+            const int64_t end = off[i] + (n * esz[i] + kPage - 1) / kPage * kPage;
             CHECK(end <= total, "array %d ends past the total", i);
             prev_end = end;
-            prev_start = off[i];
-            prev_esize = esz[i];
         }
+        CHECK(total == prev_end, "total %" PRId64 " != last end %" PRId64, total, prev_end);
     }
 }
 

@@ -288,36 +288,36 @@ def test_int32_contributions_only_in_fixed_mode():
 PAGE = 1 << 21
 
 
+ALIGN = 16 * PAGE          # every array starts on a 32 MiB boundary
+GAP = 17 * PAGE            # at least this far past the end of the previous one
+
+
 @pytest.mark.parametrize("n,W,gdt", [(875_000_000, 8, "f32"), (812_500_000, 16, "bf16"),
                                      (2_734_375_000, 8, "i32"), (1, 1, "f32"), (0, 3, "bf16"),
-                                     (3_000_001, 64, "f32")])
+                                     (3_000_001, 64, "f32"), (64 << 20, 8, "f32")])
 @pytest.mark.parametrize("opts", [dict(), dict(bf16_copy=False), dict(agg_f32=True, agg_i32=True)])
-def test_shard_layout_places_every_array_on_staggered_pages(n, W, gdt, opts):
+def test_shard_layout_places_every_array_on_32MiB_boundaries(n, W, gdt, opts):
     offs, total = dd.shard_layout(n, W, gdt, **opts)
     esize = {"f32": 4, "bf16": 2, "i32": 4}[gdt]
     want = [n * esize] * W + [4 * n] * 3 + [
         2 * n if opts.get("bf16_copy", True) else 0,
         4 * n if opts.get("agg_f32") else 0, 4 * n if opts.get("agg_i32") else 0]
-    esizes = [esize] * W + [4, 4, 4, 2, 4, 4]
     requested = [True] * (W + 3) + [opts.get("bf16_copy", True), bool(opts.get("agg_f32")),
                                     bool(opts.get("agg_i32"))]
-    placed = [(o, sz, e) for o, sz, e in zip(offs, want, esizes) if o >= 0]
     assert [o >= 0 for o in offs] == requested
-    prev_end = prev = None
-    for o, sz, e in placed:
-        assert o % PAGE == 0
-        rounded = -(-sz // PAGE) * PAGE
-        if prev_end is not None:
-            gap = (o - prev_end) // PAGE
-            assert gap in (1, 2)                 # one unused page, two to fix parity
-            if gap == 2:                         # the second page only when needed
-                assert (e == 4 and (o // PAGE - 1) % 2 == 1) or \
-                    (e == 2 and prev[1] == 2 and (o // PAGE - 1 - prev[0] // PAGE) % 2 == 0)
-        if e == 4:
-            assert (o // PAGE) % 2 == 0          # 4-byte arrays start on even pages
-        if e == 2 and prev is not None and prev[1] == 2:
-            assert ((o - prev[0]) // PAGE) % 2 == 1
-        prev_end, prev = o + rounded, (o, e)
+    if n == 0:
+        assert total == 0 and all(o == 0 for o in offs if o >= 0)
+        return
+    placed = [(o, sz) for o, sz in zip(offs, want) if o >= 0]
+    prev_end = None
+    for o, sz in placed:
+        assert o % ALIGN == 0
+        if prev_end is None:
+            assert o == 0
+        else:
+            # the first 32 MiB boundary at least 17 pages past the previous end
+            assert o >= prev_end + GAP and o - ALIGN < prev_end + GAP
+        prev_end = o + -(-sz // PAGE) * PAGE
     assert total == prev_end
 
 
@@ -339,14 +339,13 @@ def test_binding_refuses_a_call_spanning_two_gpus():
     is touched)."""
     import types
     import paper_2409_00918_amd as dd
-    import torch
-    g0 = types.SimpleNamespace(is_cuda=True, device=torch.device("cuda", 0))
-    g1 = types.SimpleNamespace(is_cuda=True, device=torch.device("cuda", 1))
-    host = types.SimpleNamespace(is_cuda=False, device=torch.device("cpu"))
-    assert dd._device([g0, None, host, g0]) == torch.device("cuda", 0)
-    assert dd._device([host, None]) is None
+    g0 = types.SimpleNamespace(get_device=lambda: 0)
+    g1 = types.SimpleNamespace(get_device=lambda: 1)
+    host = types.SimpleNamespace(get_device=lambda: -1)
+    assert dd._device_index([g0, None, host, g0]) == 0
+    assert dd._device_index([host, None]) == -1
     with pytest.raises(ValueError, match="one GPU"):
-        dd._device([g0, host, g1])
+        dd._device_index([g0, host, g1])
 
 
 def test_shard_layout_refuses_a_total_beyond_int64():
