@@ -472,6 +472,69 @@ def test_fused_on_cu_masked_streams(mode):
             hip.hipStreamDestroy(h)
 
 
+def test_concurrent_calls_from_two_threads():
+    """The library keeps no per-call state and is re-entrant: two host
+    threads (the ctypes calls release the interpreter lock) each enqueue 12
+    steps on their own stream and shard at the same time, with different
+    worker counts, modes and sizes; every result equals the same steps run
+    alone, one thread after the other."""
+    import threading
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    cases = [(8, "f32", "fp32", 1_000_003), (5, "bf16", "fixed", 777_777)]
+    inputs = []
+    for i, (W, gdtype, mode, n) in enumerate(cases):
+        gs = synth.host_grads(350 + i, 0, W, n, 1e-4, gdtype=gdtype)
+        p, m, v = synth.host_state(350 + i, n, mv_sigma=1e-4)
+        inputs.append(([to_dev(g) for g in gs], (p, m, v)))
+
+    def run(i, state, stream, barrier=None):
+        W, gdtype, mode, n = cases[i]
+        dg = inputs[i][0]
+        if barrier is not None:
+            barrier.wait()
+        with t_.cuda.stream(stream):
+            for step in range(1, 13):
+                dd.aggregate_adam(dg, *state, lr=HP["lr"], beta1=HP["beta1"], beta2=HP["beta2"],
+                                  eps=HP["eps"], weight_decay=HP["wd"], step=step, mode=mode,
+                                  frac_bits=24)
+        stream.synchronize()
+
+    def fresh(i):
+        n = cases[i][3]
+        return [to_dev(x) for x in inputs[i][1]] + [to_dev(np.zeros(n, np.uint16))]
+
+    streams = [t_.cuda.Stream(), t_.cuda.Stream()]
+    alone = []
+    for i in range(2):
+        st = fresh(i)
+        t_.cuda.synchronize()
+        run(i, st, streams[i])
+        alone.append(st)
+    together = [fresh(0), fresh(1)]
+    t_.cuda.synchronize()
+    barrier = threading.Barrier(2)
+    errors = []
+
+    def worker(i):
+        try:
+            run(i, together[i], streams[i], barrier)
+        except Exception as e:          # reported below, in the main thread
+            errors.append(e)
+
+    threads = [threading.Thread(target=worker, args=(i,)) for i in range(2)]
+    for th in threads:
+        th.start()
+    for th in threads:
+        th.join(timeout=120)
+    assert not errors, errors
+    assert not any(th.is_alive() for th in threads)
+    t_.cuda.synchronize()
+    for i in range(2):
+        for a, b in zip(alone[i], together[i]):
+            assert t_.equal(a, b), f"case {i}"
+
+
 def test_resume_from_saved_state_is_bit_identical():
     """5 steps straight equal 2 steps, a save/restore of (p, m, v, t), and 3
     more steps: all optimizer state is the caller's."""
