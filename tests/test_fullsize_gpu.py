@@ -100,3 +100,44 @@ def test_full_size_shard_sampled_parity(name):
     finally:
         del dg, dp, dm, dv, d16, dai, sh
         t_.cuda.empty_cache()
+
+
+def test_full_size_trajectory_of_40_steps():
+    """40 steps on the 7B/8 shard (fresh seeded gradients every step, the
+    launch configuration bench.py times).  The oracle runs the same 40 steps
+    on its own copy of a sampled subset of the state, from the initial state
+    only, so any difference would compound; every 8 steps the sampled p, m,
+    v and bf16 copy must match it bit for bit."""
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    wl = synth.WORKLOADS["opt7b_shard8_w8_f32"]
+    free, _ = t_.cuda.mem_get_info()
+    if bytes_needed(wl) > 0.92 * free:
+        pytest.skip("not enough device memory")
+    n, W = wl.n, wl.W
+    sh = dd.allocate_shard(n, W, wl.gdtype)
+    dp, dm, dv = synth.device_state(wl.wid, n, wl.p_sigma, out=(sh.param, sh.m, sh.v))
+    idx = np.unique(np.random.default_rng(77).integers(0, n, 1 << 16)).astype(np.int64)
+    ix = t_.from_numpy(idx).cuda()
+    p, m, v = (to_host(x[ix]) for x in (dp, dm, dv))
+    hp = dict(lr=np.float32(wl.lr), beta1=np.float32(wl.beta1), beta2=np.float32(wl.beta2),
+              eps=np.float32(wl.eps), wd=np.float32(wl.wd))
+    try:
+        for t in range(1, 41):
+            synth.device_grads(wl.wid, 100 + t, W, n, wl.sigma, outlier_frac=wl.outlier_frac,
+                               outlier_scale=wl.outlier_scale, out=sh.grads)
+            gs = [to_host(g[ix]) for g in sh.grads]
+            dd.aggregate_adam(sh.grads, dp, dm, dv, sh.param_bf16, lr=hp["lr"],
+                              beta1=hp["beta1"], beta2=hp["beta2"], eps=hp["eps"],
+                              weight_decay=hp["wd"], step=t)
+            want = oracle.fused(gs, p, m, v, t=t, **hp)
+            p, m, v = want["p"], want["m"], want["v"]
+            if t % 8 == 0:
+                t_.cuda.synchronize()
+                got = {"p": to_host(dp[ix]), "m": to_host(dm[ix]), "v": to_host(dv[ix]),
+                       "p16": to_host(sh.param_bf16[ix])}
+                assert_parity(got, want, f"trajectory step {t}")
+                print(f"[fullsize] trajectory step {t} ok", flush=True)
+    finally:
+        del dp, dm, dv, sh
+        t_.cuda.empty_cache()
