@@ -331,6 +331,74 @@ void layout_case(int W, int64_t n)
     HIP_OK(hipFree(slab));
 }
 
+// Memory from the virtual-memory API (one physical allocation mapped at a
+// reserved range, as VMM-based allocators hand it out): accepted by the
+// pointer checks and computed like any device memory.
+void vmm_case(int W, int64_t n)
+{
+    const char *label = "virtual-memory-API allocation";
+    hipMemAllocationProp prop = {};
+    prop.type = hipMemAllocationTypePinned;
+    prop.location.type = hipMemLocationTypeDevice;
+    HIP_OK(hipGetDevice(&prop.location.id));
+    size_t gran = 0;
+    HIP_OK(hipMemGetAllocationGranularity(&gran, &prop, hipMemAllocationGranularityMinimum));
+    std::vector<int64_t> off(W + 6);
+    int64_t total = 0;
+    expect(disdp_shard_layout(n, W, DISDP_DT_F32, DISDP_LAYOUT_BF16_COPY, off.data(), &total),
+           DISDP_OK, label);
+    const size_t size = (static_cast<size_t>(total) + gran - 1) / gran * gran;
+    hipMemGenericAllocationHandle_t h;
+    HIP_OK(hipMemCreate(&h, size, &prop, 0));
+    void *va = nullptr;
+    HIP_OK(hipMemAddressReserve(&va, size, 0, nullptr, 0));
+    HIP_OK(hipMemMap(va, size, 0, h, 0));
+    hipMemAccessDesc acc = {};
+    acc.location = prop.location;
+    acc.flags = hipMemAccessFlagsProtReadWrite;
+    HIP_OK(hipMemSetAccess(va, size, &acc, 1));
+    char *slab = static_cast<char *>(va);
+    HostGrads g(W, DISDP_DT_F32, n, 6262, 1e-3f);
+    std::vector<const void *> dg(W), hg(W);
+    const size_t fb = static_cast<size_t>(n) * 4;
+    for (int w = 0; w < W; ++w) {
+        dg[w] = slab + off[w];
+        hg[w] = g.ptr(w);
+        HIP_OK(hipMemcpy(slab + off[w], g.ptr(w), fb, hipMemcpyDefault));
+    }
+    std::vector<float> p(n), m(n, 0.0f), v(n, 0.0f), got(n);
+    std::vector<uint16_t> p16(n), g16(n);
+    for (int64_t i = 0; i < n; ++i)
+        p[i] = draw(6002, i, 0.02f);
+    float *dp = reinterpret_cast<float *>(slab + off[W]);
+    float *dm = reinterpret_cast<float *>(slab + off[W + 1]);
+    float *dv = reinterpret_cast<float *>(slab + off[W + 2]);
+    uint16_t *d16 = reinterpret_cast<uint16_t *>(slab + off[W + 3]);
+    HIP_OK(hipMemcpy(dp, p.data(), fb, hipMemcpyDefault));
+    HIP_OK(hipMemcpy(dm, m.data(), fb, hipMemcpyDefault));
+    HIP_OK(hipMemcpy(dv, v.data(), fb, hipMemcpyDefault));
+    Hp hh;
+    const disdp_adamw_hparams_t hp = hparams(hh, 2);
+    expect(disdp_aggregate_adam(dg.data(), W, DISDP_DT_F32, n, DISDP_AGG_FP32, 0, dp, dm, dv,
+                                d16, nullptr, nullptr, &hp, 0),
+           DISDP_OK, label);
+    HIP_OK(hipDeviceSynchronize());
+    oracle_fused(hg.data(), W, DISDP_DT_F32, n, DISDP_AGG_FP32, 0, p.data(), m.data(), v.data(),
+                 p16.data(), nullptr, nullptr, hh.lr, hh.b1, hh.b2, hh.eps, hh.wd, 2, 1.0f);
+    bool ok = true;
+    HIP_OK(hipMemcpy(got.data(), dp, fb, hipMemcpyDefault));
+    ok = same(got.data(), p.data(), fb, "p", label) && ok;
+    HIP_OK(hipMemcpy(got.data(), dm, fb, hipMemcpyDefault));
+    ok = same(got.data(), m.data(), fb, "m", label) && ok;
+    HIP_OK(hipMemcpy(g16.data(), d16, n * 2, hipMemcpyDefault));
+    ok = same(g16.data(), p16.data(), n * 2, "p16", label) && ok;
+    std::printf("%s %s: W=%d n=%lld mapped %zu bytes\n", ok ? "ok" : "FAIL", label, W,
+                static_cast<long long>(n), size);
+    HIP_OK(hipMemUnmap(va, size));
+    HIP_OK(hipMemAddressFree(va, size));
+    HIP_OK(hipMemRelease(h));
+}
+
 // Argument errors a C caller can make; none of them launches anything.
 void error_case()
 {
@@ -411,6 +479,8 @@ int main(int argc, char **argv)
     quantize_case(6, 500009, 24);
     std::fflush(stdout);
     layout_case(4, 1 << 20);
+    std::fflush(stdout);
+    vmm_case(3, 3 << 19);
     std::fflush(stdout);
     error_case();
     if (failures) {
