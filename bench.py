@@ -433,7 +433,13 @@ def run_entry(args):
                   12 + 2 written;
     two_call   -- disdp_aggregate into an fp32 aggregate, then
                   disdp_adam_step on it: the unfused path, 8 bytes per
-                  element more than the fused call."""
+                  element more than the fused call;
+    fused_graph -- the fused call as one HIP graph captured once and
+                  replayed every step: a copy node refreshes the step's
+                  constants (disdp_step_scalars, written into pinned host
+                  memory before each replay) in device memory, then
+                  disdp_aggregate_adam_dev reads them.  Same bytes as the
+                  fused call; the timed region is the replay."""
     import numpy as np
     import torch
     import paper_2409_00918_amd as dd
@@ -446,7 +452,37 @@ def run_entry(args):
     gb = 2 if wl.gdtype == "bf16" else 4
     kw = dict(lr=hp["lr"], beta1=hp["beta1"], beta2=hp["beta2"], eps=hp["eps"],
               weight_decay=hp["wd"])
-    if args.entry == "adam_step":
+    graph = None
+
+    def prepare(t):
+        pass
+
+    if args.entry == "fused_graph":
+        sh = allocate(wl)
+        bpe = dd.algorithmic_bytes_per_element(wl.W, gb)
+        host = torch.zeros(10, dtype=torch.float32, pin_memory=True)
+        dev = torch.zeros(10, dtype=torch.float32, device="cuda")
+
+        def set_step(t):
+            sc = dd.step_scalars(step=t, **kw)
+            host.copy_(torch.frombuffer(bytearray(sc), dtype=torch.float32))
+
+        torch.cuda.synchronize()
+        side = torch.cuda.Stream()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=side):
+            dev.copy_(host, non_blocking=True)
+            dd.aggregate_adam_dev(sh.grads, sh.param, sh.m, sh.v, sh.param_bf16, scalars=dev,
+                                  mode=wl.mode, frac_bits=wl.frac_bits)
+        torch.cuda.synchronize()
+
+        def prepare(t):
+            torch.cuda.synchronize()          # the previous replay has read `host`
+            set_step(t)
+
+        def call(t):
+            graph.replay()
+    elif args.entry == "adam_step":
         sh = dd.allocate_shard(wl.n, 1, "f32")
         # an aggregate-sized gradient: one draw at sqrt(W) times the spread
         synth.device_grads(wl.wid, 1, 1, wl.n, wl.sigma * wl.W ** 0.5, out=sh.grads)
@@ -478,18 +514,20 @@ def run_entry(args):
                 dd.aggregate(sh.grads, mode=wl.mode, frac_bits=wl.frac_bits,
                              agg_out_f32=None if fixed else sh.agg_f32,
                              agg_out_i32=sh.agg_i32 if fixed else None)
-    if args.entry != "aggregate":
+    if args.entry not in ("aggregate", "fused_graph"):
         synth.device_state(wl.wid, wl.n, wl.p_sigma, out=(sh.param, sh.m, sh.v))
     s = torch.cuda.current_stream()
     t = 0
     for _ in range(args.warmup):
         t += 1
+        prepare(t)
         call(t)
     torch.cuda.synchronize()
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(args.steps)]
     for a, b in ev:
         t += 1
+        prepare(t)
         a.record(s)
         call(t)
         b.record(s)
@@ -497,7 +535,8 @@ def run_entry(args):
     ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
     achieved = wl.n * bpe / (ms * 1e-3) / 1e9
     names = {"aggregate": "disdp_aggregate", "adam_step": "disdp_adam_step",
-             "two_call": "disdp_aggregate then disdp_adam_step"}
+             "two_call": "disdp_aggregate then disdp_adam_step",
+             "fused_graph": "disdp_aggregate_adam_dev replayed as a HIP graph"}
     print(json.dumps({"metric": f"G elements/s ({names[args.entry]})",
                       "value": round(wl.n / (ms * 1e-3) / 1e9, 3), "unit": "G elements/s",
                       "avg_ms": round(ms, 4), "steps": args.steps,
@@ -683,7 +722,8 @@ def main(argv=None):
                     help="p, m, v and the bf16 copy in pinned host memory")
     ap.add_argument("--contributions", choices=["float", "i32"], default="float",
                     help="i32: feed the fused call pre-quantised contributions")
-    ap.add_argument("--entry", choices=["fused", "aggregate", "adam_step", "two_call"],
+    ap.add_argument("--entry", choices=["fused", "aggregate", "adam_step", "two_call",
+                                        "fused_graph"],
                     default="fused",
                     help="time another entry point on the same shard (not the headline)")
     args = ap.parse_args(argv)

@@ -18,7 +18,11 @@
  *   disdp_quantize       -- the worker-side conversion of a gradient into the
  *                           integer format the fixed-point mode sums;
  *   disdp_shard_layout   -- where to place a shard's arrays in one
- *                           allocation for the fastest streaming.
+ *                           allocation for the fastest streaming;
+ *   disdp_step_scalars, disdp_aggregate_adam_dev
+ *                        -- the fused call with the step's constants in
+ *                           device memory, for one HIP graph replayed
+ *                           across optimizer steps.
  *
  * The calls follow the shape of the paper's asynchronous push/pull API
  * (Table II: a buffer pointer and a length; completion awaited through a
@@ -174,6 +178,43 @@ disdp_status_t disdp_aggregate_adam(const void *const *grads, int W,
                                     float *agg_out_f32, int32_t *agg_out_i32,
                                     const disdp_adamw_hparams_t *hp,
                                     hipStream_t stream);
+
+/* The per-step constants of the optimizer, as the calls above derive them
+ * from disdp_adamw_hparams_t on the host: beta1, 1 - beta1, beta2, 1 - beta2,
+ * the bias corrections 1 - beta1^t and 1 - beta2^t (double, rounded once),
+ * 1 - lr weight_decay (double, rounded once), lr, eps and grad_scale. */
+typedef struct {
+    float beta1, one_minus_beta1;
+    float beta2, one_minus_beta2;
+    float bias_correction1, bias_correction2;
+    float decay;
+    float lr, eps, grad_scale;
+} disdp_step_scalars_t;
+
+/* Fills `out` with the constants of step hp->step, exactly as
+ * disdp_aggregate_adam computes them.  Pure host computation, no HIP call.
+ * Returns DISDP_ERR_INVALID_ARG for NULL pointers or invalid
+ * hyperparameters (the ranges of disdp_adamw_hparams_t). */
+disdp_status_t disdp_step_scalars(const disdp_adamw_hparams_t *hp, disdp_step_scalars_t *out);
+
+/* disdp_aggregate_adam with the step constants read from memory when the
+ * kernel runs instead of when the call is made: `scalars` points to a
+ * disdp_step_scalars_t in device memory (or pinned host memory mapped for
+ * the device), 4-byte aligned, filled by disdp_step_scalars; it must not
+ * overlap an output (DISDP_ERR_ALIAS).  For HIP graphs: a captured
+ * graph whose copy node refreshes `scalars` from a host buffer that the
+ * caller rewrites before each replay serves every optimizer step with one
+ * capture, and gives the same bits as disdp_aggregate_adam with that step's
+ * hyperparameters.  The contents of `scalars` are not checked (the pointer
+ * is); every other argument as in disdp_aggregate_adam. */
+disdp_status_t disdp_aggregate_adam_dev(const void *const *grads, int W,
+                                        disdp_dtype_t gdtype, int64_t n,
+                                        disdp_agg_mode_t mode, int frac_bits,
+                                        float *param, float *m, float *v,
+                                        uint16_t *param_bf16_out,
+                                        float *agg_out_f32, int32_t *agg_out_i32,
+                                        const disdp_step_scalars_t *scalars,
+                                        hipStream_t stream);
 
 /* The float-to-integer format conversion a worker's NIC applies before
  * pushing its gradient to an integer-only switch (Section III-B "Format

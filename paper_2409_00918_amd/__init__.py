@@ -16,6 +16,9 @@ call raises.
 ``quantize``        -- a worker's float -> int32 conversion (disdp_quantize)
 ``allocate_shard``  -- one device allocation holding a shard's arrays, placed
                        by disdp_shard_layout
+``aggregate_adam_dev``, ``step_scalars``
+                    -- the fused call with the step's constants read from
+                       device memory (one HIP graph for every step)
 """
 from __future__ import annotations
 
@@ -33,7 +36,8 @@ AGG_FP32, AGG_FIXED = 0, 1
 MAX_W = 64
 
 EXPORTS = ("disdp_aggregate", "disdp_adam_step", "disdp_aggregate_adam",
-           "disdp_quantize", "disdp_shard_layout", "disdp_status_string")
+           "disdp_quantize", "disdp_shard_layout", "disdp_step_scalars",
+           "disdp_aggregate_adam_dev", "disdp_status_string")
 LAYOUT_BF16_COPY, LAYOUT_AGG_F32, LAYOUT_AGG_I32 = 1, 2, 4
 
 
@@ -42,6 +46,15 @@ class AdamWHParams(ctypes.Structure):
     _fields_ = [("lr", ctypes.c_float), ("beta1", ctypes.c_float),
                 ("beta2", ctypes.c_float), ("eps", ctypes.c_float),
                 ("weight_decay", ctypes.c_float), ("step", ctypes.c_int64),
+                ("grad_scale", ctypes.c_float)]
+
+
+class StepScalars(ctypes.Structure):
+    """disdp_step_scalars_t: the per-step constants of the optimizer."""
+    _fields_ = [("beta1", ctypes.c_float), ("one_minus_beta1", ctypes.c_float),
+                ("beta2", ctypes.c_float), ("one_minus_beta2", ctypes.c_float),
+                ("bias_correction1", ctypes.c_float), ("bias_correction2", ctypes.c_float),
+                ("decay", ctypes.c_float), ("lr", ctypes.c_float), ("eps", ctypes.c_float),
                 ("grad_scale", ctypes.c_float)]
 
 
@@ -97,6 +110,11 @@ def lib() -> ctypes.CDLL:
         L.disdp_quantize.argtypes = [vp, ci, i64, ci, vp, vp]
         L.disdp_shard_layout.restype = ci
         L.disdp_shard_layout.argtypes = [i64, ci, ci, ctypes.c_uint, vp, vp]
+        L.disdp_step_scalars.restype = ci
+        L.disdp_step_scalars.argtypes = [ctypes.POINTER(AdamWHParams), ctypes.POINTER(StepScalars)]
+        L.disdp_aggregate_adam_dev.restype = ci
+        L.disdp_aggregate_adam_dev.argtypes = [vp, ci, ci, i64, ci, ci, vp, vp, vp, vp, vp, vp,
+                                               vp, vp]
         L.disdp_status_string.restype = ctypes.c_char_p
         L.disdp_status_string.argtypes = [ci]
         _lib = L
@@ -143,6 +161,15 @@ def raw_aggregate_adam(grad_ptrs, W, gdtype, n, mode, frac_bits, param, m, v,
         arr, W, gdtype, n, mode, frac_bits, param or None, m or None,
         v or None, p16 or None, agg_f32 or None, agg_i32 or None,
         None if hp is None else ctypes.byref(hp), stream or None)
+
+
+def raw_aggregate_adam_dev(grad_ptrs, W, gdtype, n, mode, frac_bits, param, m, v,
+                           p16, agg_f32, agg_i32, scalars, stream) -> int:
+    arr = None if grad_ptrs is None else _ptr_array(grad_ptrs)
+    return lib().disdp_aggregate_adam_dev(
+        arr, W, gdtype, n, mode, frac_bits, param or None, m or None,
+        v or None, p16 or None, agg_f32 or None, agg_i32 or None, scalars or None,
+        stream or None)
 
 
 # --------------------------------------------------------- torch tensors --
@@ -307,6 +334,40 @@ def aggregate_adam(grads, param, m, v, param_bf16_out=None, *, lr, beta1,
         _dev_ptr(agg_out_i32, "agg_out_i32", n, (torch.int32,)),
         _hparams(lr, beta1, beta2, eps, weight_decay, step, grad_scale))
     _check(st, "disdp_aggregate_adam")
+
+
+def step_scalars(*, lr, beta1, beta2, eps, weight_decay, step, grad_scale=1.0) -> StepScalars:
+    """The constants disdp_aggregate_adam derives for this step (host)."""
+    out = StepScalars()
+    st = lib().disdp_step_scalars(
+        ctypes.byref(_hparams(lr, beta1, beta2, eps, weight_decay, step, grad_scale)),
+        ctypes.byref(out))
+    _check(st, "disdp_step_scalars")
+    return out
+
+
+def aggregate_adam_dev(grads, param, m, v, param_bf16_out=None, *, scalars,
+                       mode="fp32", frac_bits: int = 0, agg_out_f32=None,
+                       agg_out_i32=None, stream=None) -> None:
+    """aggregate_adam with the step constants read when the kernel runs from
+    `scalars`: a float32 tensor of 10 elements (a StepScalars image, e.g.
+    filled by copying step_scalars(...)), on the device or pinned host
+    memory.  Lets one captured HIP graph serve every step."""
+    torch = _torch()
+    grads, ptrs, gdt, n = _grads(grads)
+    f32 = (torch.float32,)
+    st = _launch(
+        raw_aggregate_adam_dev,
+        grads + [param, m, v, param_bf16_out, agg_out_f32, agg_out_i32, scalars], stream,
+        ptrs, len(grads), gdt, n, _mode(mode), frac_bits,
+        _dev_ptr(param, "param", n, f32), _dev_ptr(m, "m", n, f32),
+        _dev_ptr(v, "v", n, f32),
+        _dev_ptr(param_bf16_out, "param_bf16_out", n,
+                 (torch.bfloat16, torch.int16, torch.uint16)),
+        _dev_ptr(agg_out_f32, "agg_out_f32", n, f32),
+        _dev_ptr(agg_out_i32, "agg_out_i32", n, (torch.int32,)),
+        _dev_ptr(scalars, "scalars", ctypes.sizeof(StepScalars) // 4, f32))
+    _check(st, "disdp_aggregate_adam_dev")
 
 
 def quantize(grad, out, *, frac_bits: int, stream=None) -> None:

@@ -5,10 +5,21 @@
 #include "disdp.h"
 
 #include <cmath>
+#include <cstddef>
 #include <cstdint>
 #include <cstring>
 
 #include "disdp_launch.h"
+
+// disdp_step_scalars_t is the public image of the kernels' StepScalars.
+static_assert(sizeof(disdp_step_scalars_t) == sizeof(disdp::StepScalars),
+              "step scalars layout");
+static_assert(offsetof(disdp_step_scalars_t, bias_correction1) ==
+                      offsetof(disdp::StepScalars, bc1) &&
+                  offsetof(disdp_step_scalars_t, decay) == offsetof(disdp::StepScalars, decay) &&
+                  offsetof(disdp_step_scalars_t, grad_scale) ==
+                      offsetof(disdp::StepScalars, grad_scale),
+              "step scalars layout");
 
 namespace {
 
@@ -145,12 +156,13 @@ disdp_status_t run(const void *const *grads, int W, int gdtype, int64_t n,
                    int mode, int frac_bits, float *param, float *m, float *v,
                    uint16_t *p16, float *agg_f32, int32_t *agg_i32,
                    const disdp_adamw_hparams_t *hp, bool adam,
-                   bool agg_f32_required, hipStream_t stream)
+                   bool agg_f32_required, hipStream_t stream,
+                   bool scalars_in_memory = false, const disdp::StepScalars *s_dev = nullptr)
 {
     disdp_status_t st = check_counts(W, gdtype, n, mode, frac_bits);
     if (st != DISDP_OK)
         return st;
-    if (adam && (st = check_hparams(hp)) != DISDP_OK)
+    if (adam && !scalars_in_memory && (st = check_hparams(hp)) != DISDP_OK)
         return st;
     if (mode == DISDP_AGG_FP32 && agg_i32)
         return DISDP_ERR_INVALID_ARG;  // an int32 aggregate exists only in fixed mode
@@ -164,6 +176,8 @@ disdp_status_t run(const void *const *grads, int W, int gdtype, int64_t n,
         if (!grads[w])
             return DISDP_ERR_INVALID_ARG;
     if (adam && (!param || !m || !v))
+        return DISDP_ERR_INVALID_ARG;
+    if (scalars_in_memory && (!s_dev || (reinterpret_cast<uintptr_t>(s_dev) & 3)))
         return DISDP_ERR_INVALID_ARG;
     if (!adam) {
         if (agg_f32_required && !agg_f32)
@@ -189,6 +203,8 @@ disdp_status_t run(const void *const *grads, int W, int gdtype, int64_t n,
         for (int w = 0; w < W; ++w)
             if (overlaps(outs[i], span_of(grads[w], n, gb)))
                 return DISDP_ERR_ALIAS;
+        if (s_dev && overlaps(outs[i], span_of(s_dev, 1, sizeof(disdp::StepScalars))))
+            return DISDP_ERR_ALIAS;
     }
 
     // Every array must be addressable by the GPU as given (first HIP call).
@@ -197,7 +213,8 @@ disdp_status_t run(const void *const *grads, int W, int gdtype, int64_t n,
             return DISDP_ERR_INVALID_ARG;
     for (const void *p : {static_cast<const void *>(param), static_cast<const void *>(m),
                           static_cast<const void *>(v), static_cast<const void *>(p16),
-                          static_cast<const void *>(agg_f32), static_cast<const void *>(agg_i32)})
+                          static_cast<const void *>(agg_f32), static_cast<const void *>(agg_i32),
+                          static_cast<const void *>(s_dev)})
         if (p && !gpu_addressable(p))
             return DISDP_ERR_INVALID_ARG;
 
@@ -218,8 +235,9 @@ disdp_status_t run(const void *const *grads, int W, int gdtype, int64_t n,
     a.frac_bits = (mode == DISDP_AGG_FIXED) ? frac_bits : 0;
     a.qscale = std::ldexp(1.0f, a.frac_bits);
     a.dqscale = std::ldexp(1.0f, -a.frac_bits);
-    if (adam)
+    if (adam && !s_dev)
         a.s = step_scalars(hp);
+    a.s_dev = s_dev;
 
     // Vector kernels move 4 elements per lane: 16-byte groups of 4-byte
     // arrays, 8-byte groups of 2-byte arrays.  Arrays that all start the same
@@ -299,6 +317,33 @@ disdp_status_t disdp_aggregate_adam(const void *const *grads, int W,
     return run(grads, W, gdtype, n, mode, frac_bits, param, m, v, param_bf16_out,
                agg_out_f32, agg_out_i32, hp, /*adam=*/true,
                /*agg_f32_required=*/false, stream);
+}
+
+disdp_status_t disdp_step_scalars(const disdp_adamw_hparams_t *hp, disdp_step_scalars_t *out)
+{
+    if (!out)
+        return DISDP_ERR_INVALID_ARG;
+    const disdp_status_t st = check_hparams(hp);
+    if (st != DISDP_OK)
+        return st;
+    const disdp::StepScalars sc = step_scalars(hp);
+    std::memcpy(out, &sc, sizeof sc);
+    return DISDP_OK;
+}
+
+disdp_status_t disdp_aggregate_adam_dev(const void *const *grads, int W,
+                                        disdp_dtype_t gdtype, int64_t n,
+                                        disdp_agg_mode_t mode, int frac_bits,
+                                        float *param, float *m, float *v,
+                                        uint16_t *param_bf16_out, float *agg_out_f32,
+                                        int32_t *agg_out_i32,
+                                        const disdp_step_scalars_t *scalars,
+                                        hipStream_t stream)
+{
+    return run(grads, W, gdtype, n, mode, frac_bits, param, m, v, param_bf16_out,
+               agg_out_f32, agg_out_i32, nullptr, /*adam=*/true,
+               /*agg_f32_required=*/false, stream, /*scalars_in_memory=*/true,
+               reinterpret_cast<const disdp::StepScalars *>(scalars));
 }
 
 disdp_status_t disdp_quantize(const void *grad, disdp_dtype_t gdtype, int64_t n,

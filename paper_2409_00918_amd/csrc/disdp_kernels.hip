@@ -195,6 +195,13 @@ __device__ __forceinline__ int32_t saturate32(int64_t s)
     return static_cast<int32_t>(hi < INT32_MIN ? int64_t(INT32_MIN) : hi);
 }
 
+// The step constants of a launch: by value in the arguments, or read from
+// memory when the kernel runs (one uniform load per wave, scalar cache).
+__device__ __forceinline__ StepScalars step_scalars_of(const LaunchArgs &a)
+{
+    return a.s_dev ? *a.s_dev : a.s;
+}
+
 // One AdamW step on one element (decoupled decay, bias-corrected moments,
 // eps outside the square root).  `/` and sqrtf are the correctly rounded
 // IEEE operations on this target.
@@ -323,9 +330,10 @@ __device__ __forceinline__ void finish_group(const LaunchArgs &a, int64_t grp, c
         float p[4] = {P.x, P.y, P.z, P.w};
         float m[4] = {M.x, M.y, M.z, M.w};
         float v[4] = {V.x, V.y, V.z, V.w};
+        const StepScalars sc = step_scalars_of(a);
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-            adamw(a.s, agg[e], p[e], m[e], v[e]);
+            adamw(sc, agg[e], p[e], m[e], v[e]);
         st_nt(reinterpret_cast<f32x4 *>(a.p) + grp, f32x4{p[0], p[1], p[2], p[3]});
         st_nt(reinterpret_cast<f32x4 *>(a.m) + grp, f32x4{m[0], m[1], m[2], m[3]});
         st_nt(reinterpret_cast<f32x4 *>(a.v) + grp, f32x4{v[0], v[1], v[2], v[3]});
@@ -434,7 +442,7 @@ __device__ __forceinline__ void process_element(const LaunchArgs &a, int64_t i)
     }
     if constexpr (ADAM) {
         float p = a.p[i], m = a.m[i], v = a.v[i];
-        adamw(a.s, agg, p, m, v);
+        adamw(step_scalars_of(a), agg, p, m, v);
         a.p[i] = p;
         a.m[i] = m;
         a.v[i] = v;

@@ -35,6 +35,8 @@ struct LaunchArgs {
     int W, gdtype, mode, frac_bits;
     float qscale, dqscale; // 2^k and 2^-k (fixed mode)
     StepScalars s;
+    const StepScalars *s_dev;  // when set, the step constants are read here
+                               // when the kernel runs, and `s` is unused
 };
 
 // Enqueues the kernel for `a` on `stream`.  `vector_path` selects the

@@ -7,7 +7,8 @@
 //   * disdp_shard_layout over random n (up to 2^56), W, dtypes and flags:
 //     status, and every placement invariant of a successful layout;
 //   * each entry point with exactly one argument error injected into an
-//     otherwise valid call: the documented status, and no launch;
+//     otherwise valid call: the documented status, and no launch (valid
+//     fused calls: the step constants passed by value, or by address only);
 //   * valid calls whose arrays share, or do not share, a misalignment: the
 //     vector/element choice, the head of elements done one by one and the
 //     advanced pointers.
@@ -167,7 +168,8 @@ void fuzz_layout(int iters)
 
 // ---- one error injected into a valid call ---------------------------------------
 struct Call {
-    int entry;  // 0 aggregate, 1 adam_step, 2 aggregate_adam, 3 quantize
+    int entry;  // 0 aggregate, 1 adam_step, 2 aggregate_adam, 3 quantize,
+                // 4 aggregate_adam_dev
     int W, gdt, mode, k;
     int64_t n;
     const void *g[disdp::kMaxW];
@@ -177,7 +179,10 @@ struct Call {
     int32_t *ai;
     disdp_adamw_hparams_t hp;
     bool hp_null;
+    const disdp_step_scalars_t *s;  // aggregate_adam_dev
 };
+
+bool fused(int entry) { return entry == 2 || entry == 4; }
 
 // Fake, never dereferenced, well separated addresses: array i at base + i * 2^40.
 char *fake(int i) { return reinterpret_cast<char *>((uintptr_t(1) << 44) + (uintptr_t(i) << 40)); }
@@ -202,11 +207,12 @@ Call valid_call(int entry)
     c.p16 = below(2) ? reinterpret_cast<uint16_t *>(fake(73)) : nullptr;
     c.af = reinterpret_cast<float *>(fake(74));
     c.ai = c.mode == DISDP_AGG_FIXED ? reinterpret_cast<int32_t *>(fake(75)) : nullptr;
-    if (entry == 2 && below(2)) {
+    if (fused(entry) && below(2)) {
         c.af = nullptr;
         c.ai = nullptr;
     }
     c.hp = {1e-4f, 0.9f, 0.95f, 1e-8f, 0.1f, 1 + below(100000), 1.0f};
+    c.s = reinterpret_cast<const disdp_step_scalars_t *>(fake(76) + 4 * below(1000));
     return c;
 }
 
@@ -224,6 +230,10 @@ disdp_status_t issue(const Call &c)
         return disdp_aggregate_adam(c.grads, c.W, static_cast<disdp_dtype_t>(c.gdt), c.n,
                                     static_cast<disdp_agg_mode_t>(c.mode), c.k, c.p, c.m, c.v,
                                     c.p16, c.af, c.ai, hp, nullptr);
+    case 4:
+        return disdp_aggregate_adam_dev(c.grads, c.W, static_cast<disdp_dtype_t>(c.gdt), c.n,
+                                        static_cast<disdp_agg_mode_t>(c.mode), c.k, c.p, c.m,
+                                        c.v, c.p16, c.af, c.ai, c.s, nullptr);
     default:
         return disdp_quantize(c.grads ? c.grads[0] : nullptr,
                               static_cast<disdp_dtype_t>(c.gdt), c.n, c.k,
@@ -234,21 +244,21 @@ disdp_status_t issue(const Call &c)
 void fuzz_errors(int iters)
 {
     for (int it = 0; it < iters; ++it) {
-        const int entry = static_cast<int>(below(4));
+        const int entry = static_cast<int>(below(5));
         Call c = valid_call(entry);
         if (entry == 0 && c.mode == DISDP_AGG_FP32 && !c.af)
             c.af = reinterpret_cast<float *>(fake(74));
         if (entry == 0 && c.mode == DISDP_AGG_FIXED && !c.af && !c.ai)
             c.ai = reinterpret_cast<int32_t *>(fake(75));
         disdp_status_t want = DISDP_OK;
-        const int kind = static_cast<int>(below(12));
+        const int kind = static_cast<int>(below(14));
         switch (kind) {
         case 0:  // n out of range
             c.n = below(2) ? -1 - below(100) : (int64_t(1) << 56) + 1 + below(100);
             want = DISDP_ERR_INVALID_ARG;
             break;
         case 1:  // W out of range (the two single-buffer calls have none)
-            if (entry == 0 || entry == 2) {
+            if (entry == 0 || fused(entry)) {
                 c.W = below(2) ? 0 : 65 + static_cast<int>(below(100));
                 want = DISDP_ERR_INVALID_ARG;
             }
@@ -268,7 +278,7 @@ void fuzz_errors(int iters)
                 want = DISDP_ERR_INVALID_ARG;
             }
             break;
-        case 4:  // bad hyperparameters
+        case 4:  // bad hyperparameters (aggregate_adam_dev reads none)
             if (entry == 1 || entry == 2) {
                 switch (below(7)) {
                 case 0: c.hp.step = -below(5); break;
@@ -290,7 +300,7 @@ void fuzz_errors(int iters)
             want = DISDP_ERR_INVALID_ARG;
             break;
         case 6:  // NULL state
-            if (entry == 1 || entry == 2) {
+            if (entry == 1 || fused(entry)) {
                 c.m = nullptr;
                 want = DISDP_ERR_INVALID_ARG;
             }
@@ -301,7 +311,7 @@ void fuzz_errors(int iters)
                     static_cast<const char *>(c.g[below(c.W)]) +
                     (c.gdt == DISDP_DT_BF16 ? 2 : 4) * below(c.n)));
                 want = DISDP_ERR_ALIAS;
-            } else if (entry == 1 || entry == 2) {
+            } else if (entry == 1 || fused(entry)) {
                 c.v = reinterpret_cast<float *>(const_cast<char *>(
                     static_cast<const char *>(c.g[below(c.W)]) + 2 * below(c.n)));
                 want = DISDP_ERR_ALIAS;
@@ -312,13 +322,13 @@ void fuzz_errors(int iters)
             }
             break;
         case 8:  // two outputs overlapping
-            if (entry == 1 || entry == 2) {
+            if (entry == 1 || fused(entry)) {
                 c.p = c.m + below(c.n);
                 want = DISDP_ERR_ALIAS;
             }
             break;
         case 9:  // an int32 aggregate in fp32 mode
-            if ((entry == 0 || entry == 2) && c.mode == DISDP_AGG_FP32) {
+            if ((entry == 0 || fused(entry)) && c.mode == DISDP_AGG_FP32) {
                 c.ai = reinterpret_cast<int32_t *>(fake(75));
                 want = DISDP_ERR_INVALID_ARG;
             }
@@ -326,6 +336,25 @@ void fuzz_errors(int iters)
         case 10:  // memory the GPU cannot address
             g_addressable = false;
             want = DISDP_ERR_INVALID_ARG;
+            break;
+        case 12:  // step scalars missing or not 4-byte aligned
+            if (entry == 4) {
+                c.s = below(2) ? nullptr
+                               : reinterpret_cast<const disdp_step_scalars_t *>(
+                                     reinterpret_cast<const char *>(c.s) + 1 + below(3));
+                want = DISDP_ERR_INVALID_ARG;
+            }
+            break;
+        case 13:  // step scalars overlapping an output (the first or last bytes of one)
+            if (entry == 4) {
+                const int64_t nb = 4 * c.n;
+                const int64_t at = below(2) ? 4 * below(c.n < 10 ? c.n : 10)
+                                            : nb - 4 * (1 + below(c.n < 10 ? c.n : 10));
+                float *out = below(2) ? c.p : c.v;
+                c.s = reinterpret_cast<const disdp_step_scalars_t *>(
+                    reinterpret_cast<const char *>(out) + at);
+                want = DISDP_ERR_ALIAS;
+            }
             break;
         default:  // empty shard: accepted, nothing launched
             c.n = 0;
@@ -341,6 +370,17 @@ void fuzz_errors(int iters)
         const bool launched = g_launches != launches;
         CHECK(launched == (want == DISDP_OK && c.n > 0),
               "entry %d kind %d: launched=%d", entry, kind, launched);
+        if (launched && fused(entry)) {
+            // the constants travel by value, or only their address does
+            const disdp::StepScalars zero{};
+            if (entry == 4)
+                CHECK(g_args.s_dev == reinterpret_cast<const disdp::StepScalars *>(c.s) &&
+                          std::memcmp(&g_args.s, &zero, sizeof zero) == 0,
+                      "aggregate_adam_dev: scalars not passed by address only");
+            else
+                CHECK(!g_args.s_dev && g_args.s.b1 == c.hp.beta1 && g_args.s.lr == c.hp.lr,
+                      "aggregate_adam: scalars not passed by value");
+        }
         CHECK(std::strlen(disdp_status_string(st)) > 0, "empty status string");
     }
     for (int s = -5; s < 10; ++s)

@@ -357,3 +357,71 @@ def test_shard_layout_refuses_a_total_beyond_int64():
     assert ei.value.status == dd.ERR_INVALID_ARG
     offs, total = dd.shard_layout(1 << 56, 1, "bf16")
     assert 0 < total < 2 ** 63 and offs[1] >= (1 << 57)
+
+
+# ------------------------------------------------- step scalars in memory --
+def test_step_scalars_struct_layout_matches_c():
+    assert ctypes.sizeof(dd.StepScalars) == 40
+    assert dd.StepScalars.decay.offset == 24
+    assert dd.StepScalars.grad_scale.offset == 36
+
+
+@pytest.mark.parametrize("b1,b2,lr,wd", [(0.9, 0.95, 1e-4, 0.1), (0.9, 0.999, 3e-4, 0.0),
+                                         (0.5, 0.5, 1.0, 0.25), (0.0, 0.0, 1e-3, 0.01),
+                                         (0.99, 0.9999, 6e-5, 1.0)])
+@pytest.mark.parametrize("t", [1, 2, 3, 17, 1000, 10**6, 2**40])
+def test_step_scalars_equal_the_oracles(b1, b2, lr, wd, t):
+    np = pytest.importorskip("numpy")
+    import oracle
+    f = np.float32
+    got = dd.step_scalars(lr=f(lr), beta1=f(b1), beta2=f(b2), eps=f(1e-8),
+                          weight_decay=f(wd), step=t, grad_scale=f(0.5))
+    want = oracle.scalars(f(lr), f(b1), f(b2), f(wd), t)
+    bits = np.array([got.beta1, got.one_minus_beta1, got.beta2, got.one_minus_beta2,
+                     got.bias_correction1, got.bias_correction2, got.decay], dtype=np.float32)
+    assert np.array_equal(bits.view(np.uint32), want.view(np.uint32))
+    assert (got.lr, got.eps, got.grad_scale) == (f(lr), f(1e-8), f(0.5))
+
+
+def test_step_scalars_argument_checks():
+    out = dd.StepScalars()
+    L = dd.lib()
+    assert L.disdp_step_scalars(None, ctypes.byref(out)) == dd.ERR_INVALID_ARG
+    assert L.disdp_step_scalars(ctypes.byref(hp()), None) == dd.ERR_INVALID_ARG
+    assert L.disdp_step_scalars(ctypes.byref(hp(step=0)), ctypes.byref(out)) == dd.ERR_INVALID_ARG
+    assert L.disdp_step_scalars(ctypes.byref(hp(beta1=1.0)), ctypes.byref(out)) == \
+        dd.ERR_INVALID_ARG
+    with pytest.raises(dd.DisdpError):
+        dd.step_scalars(lr=1e-4, beta1=0.9, beta2=0.95, eps=-1.0, weight_decay=0.0, step=1)
+
+
+def fused_dev(ptrs=None, W=8, gdtype=dd.DT_F32, n=N, mode=dd.AGG_FP32, k=24,
+              p=A[70], m=A[71], v=A[72], p16=A[73], f32=0, i32=0, s=A[75]):
+    if ptrs is None:
+        ptrs = A[:W]
+    elif ptrs is NULL_ARRAY:
+        ptrs = None
+    return dd.raw_aggregate_adam_dev(ptrs, W, gdtype, n, mode, k, p, m, v, p16,
+                                     f32, i32, s, 0)
+
+
+def test_fused_dev_argument_checks():
+    assert fused_dev(W=0) == dd.ERR_INVALID_ARG
+    assert fused_dev(n=-1) == dd.ERR_INVALID_ARG
+    assert fused_dev(gdtype=9) == dd.ERR_UNSUPPORTED
+    assert fused_dev(mode=dd.AGG_FIXED, k=31) == dd.ERR_INVALID_ARG
+    assert fused_dev(i32=A[74]) == dd.ERR_INVALID_ARG    # int32 aggregate in fp32 mode
+    assert fused_dev(s=0) == dd.ERR_INVALID_ARG          # no scalars
+    assert fused_dev(s=A[75] + 2) == dd.ERR_INVALID_ARG  # misaligned scalars
+    assert fused_dev(v=0) == dd.ERR_INVALID_ARG
+    assert fused_dev(ptrs=NULL_ARRAY, p=0, m=0, v=0, p16=0, s=0, n=0) == dd.OK
+
+
+def test_fused_dev_aliasing():
+    assert fused_dev(s=A[70] + 4 * (N - 4)) == dd.ERR_ALIAS   # scalars inside the weights
+    assert fused_dev(s=A[70] + 4 * N - 36) == dd.ERR_ALIAS    # straddling their end
+    assert fused_dev(s=A[73] + 2 * N - 4) == dd.ERR_ALIAS     # end of the bf16 copy
+    assert fused_dev(p=A[3]) == dd.ERR_ALIAS
+    # scalars overlapping a contribution are legal (both are read only); the
+    # call then fails later on the fake, unmapped addresses
+    assert fused_dev(s=A[2] + 8) == dd.ERR_INVALID_ARG

@@ -422,6 +422,106 @@ def test_fused_call_captured_in_a_hip_graph(mode):
     del graph
 
 
+def _scalars_tensor(**kw):
+    """The StepScalars image of one step as 10 float32 values (host)."""
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    return t_.frombuffer(bytearray(dd.step_scalars(**kw)), dtype=t_.float32).clone()
+
+
+@pytest.mark.parametrize("gdtype", ["f32", "bf16"])
+@pytest.mark.parametrize("mode", ["fp32", "fixed"])
+def test_fused_dev_equals_fused(gdtype, mode):
+    """disdp_aggregate_adam_dev, with the step's constants in device memory
+    and in pinned host memory, gives the bits of disdp_aggregate_adam with
+    the same hyperparameters, over ragged lengths, steps and settings."""
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    settings = [dict(lr=HP["lr"], beta1=HP["beta1"], beta2=HP["beta2"], eps=HP["eps"],
+                     weight_decay=HP["wd"], step=1),
+                dict(lr=np.float32(3e-3), beta1=np.float32(0.8), beta2=np.float32(0.999),
+                     eps=np.float32(1e-6), weight_decay=np.float32(0.0), step=7,
+                     grad_scale=np.float32(0.125)),
+                dict(lr=np.float32(1e-5), beta1=np.float32(0.9), beta2=np.float32(0.95),
+                     eps=np.float32(1e-8), weight_decay=np.float32(1.0), step=123_456)]
+    for i, n in enumerate([1, 5, 257, 4099, 300_007]):
+        for j, kw in enumerate(settings):
+            W = (3, 8, 5)[j]
+            gs = synth.host_grads(900 + i, j, W, n, 1e-4, gdtype=gdtype,
+                                  outlier_frac=0.01, outlier_scale=100.0)
+            p, m, v = synth.host_state(900 + i, n, mv_sigma=1e-4)
+            dg = [to_dev(g) for g in gs]
+            ref = [to_dev(x) for x in (p, m, v)] + [to_dev(np.zeros(n, np.uint16))]
+            dd.aggregate_adam(dg, *ref, mode=mode, frac_bits=20, **kw)
+            for where in ("device", "pinned"):
+                sc = _scalars_tensor(**kw)
+                sc = sc.cuda() if where == "device" else sc.pin_memory()
+                got = [to_dev(x) for x in (p, m, v)] + [to_dev(np.zeros(n, np.uint16))]
+                dd.aggregate_adam_dev(dg, *got, scalars=sc, mode=mode, frac_bits=20)
+                t_.cuda.synchronize()
+                for a, b in zip(got, ref):
+                    assert t_.equal(a, b), _label(n=n, setting=j, where=where)
+            if n == 4099:
+                want = oracle.fused(gs, p, m, v, mode=oracle.AGG_FIXED if mode == "fixed"
+                                    else oracle.AGG_FP32, frac_bits=20, t=kw["step"],
+                                    lr=kw["lr"], beta1=kw["beta1"], beta2=kw["beta2"],
+                                    eps=kw["eps"], wd=kw["weight_decay"],
+                                    grad_scale=kw.get("grad_scale", np.float32(1.0)))
+                assert_parity({"p": to_host(ref[0]), "m": to_host(ref[1]),
+                               "v": to_host(ref[2]), "p16": to_host(ref[3])}, want,
+                              _label(n=n, setting=j))
+
+
+@pytest.mark.parametrize("mode", ["fp32", "fixed"])
+def test_one_hip_graph_serves_every_optimizer_step(mode):
+    """One capture, six optimizer steps: the graph holds a copy node that
+    refreshes the step's constants in device memory from pinned host memory
+    (rewritten before each replay) and the disdp_aggregate_adam_dev launch.
+    Fresh contributions are written into the captured buffers between
+    replays, with unrelated eager work and synchronisations in between; each
+    step must equal the oracle's step t bit for bit."""
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    n, W = 300_007, 4
+    kw = dict(lr=HP["lr"], beta1=HP["beta1"], beta2=HP["beta2"], eps=HP["eps"],
+              weight_decay=HP["wd"])
+    p, m, v = synth.host_state(910, n, mv_sigma=1e-4)
+    dg = [t_.zeros(n, device="cuda") for _ in range(W)]
+    st = [to_dev(x) for x in (p, m, v)] + [to_dev(np.zeros(n, np.uint16))]
+    agg = t_.zeros(n, dtype=t_.int32, device="cuda") if mode == "fixed" else None
+    host = t_.zeros(10, dtype=t_.float32, pin_memory=True)
+    dev = t_.zeros(10, dtype=t_.float32, device="cuda")
+    t_.cuda.synchronize()
+    side = t_.cuda.Stream()
+    graph = t_.cuda.CUDAGraph()
+    with t_.cuda.graph(graph, stream=side):
+        dev.copy_(host, non_blocking=True)
+        dd.aggregate_adam_dev(dg, *st, scalars=dev, mode=mode, frac_bits=24,
+                              agg_out_i32=agg)
+    t_.cuda.synchronize()
+    assert t_.equal(st[0].cpu(), t_.from_numpy(p))     # capture ran nothing
+    other = t_.zeros(1 << 20, device="cuda")
+    for t in range(1, 7):
+        gs = synth.host_grads(910, t, W, n, 1e-4, outlier_frac=0.01, outlier_scale=100.0)
+        for d, g in zip(dg, gs):
+            d.copy_(t_.from_numpy(g))
+        host.copy_(_scalars_tensor(step=t, **kw))
+        t_.cuda.synchronize()
+        graph.replay()
+        t_.cuda.synchronize()
+        other.add_(1.0)
+        t_.cuda.synchronize()
+        want = oracle.fused(gs, p, m, v, mode=oracle.AGG_FIXED if mode == "fixed"
+                            else oracle.AGG_FP32, frac_bits=24, t=t,
+                            want_agg_i32=mode == "fixed", **HP)
+        assert_parity({"p": to_host(st[0]), "m": to_host(st[1]), "v": to_host(st[2]),
+                       "p16": to_host(st[3])}, want, f"graph step {t} {mode}")
+        if mode == "fixed":
+            assert np.array_equal(to_host(agg), want["agg_i32"]), f"step {t} agg_i32"
+        p, m, v = want["p"], want["m"], want["v"]
+    del graph
+
+
 def _cu_masked_stream(n_cus):
     """A default-priority stream restricted to the first n_cus CUs
     (hipExtStreamCreateWithCUMask on torch's HIP runtime)."""
