@@ -687,6 +687,18 @@ int resident_blocks_per_cu(const void *fn, int lds_bytes)
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
+// A dispatch counts its work-items in 32 bits per dimension, so a grid of
+// `block`-lane blocks holds at most (2^32 - 1) / block of them.  Every
+// kernel here walks its work grid-stride, so a clamped grid still covers a
+// shard of any accepted size (beyond 2^34 elements for the one-tile-per-
+// block grids).
+constexpr int64_t kMaxGridLanes = 0xffffffffLL;
+int64_t clamp_grid(int64_t blocks, int block)
+{
+    const int64_t max_blocks = kMaxGridLanes / block;
+    return blocks < 1 ? 1 : blocks > max_blocks ? max_blocks : blocks;
+}
+
 // `work_blocks`: blocks needed for one tile (or element chunk) each;
 // `lds_bytes`: dynamic LDS reserved per block (an occupancy cap).
 hipError_t launch_kernel(const void *fn, int64_t work_blocks, bool persistent, const LaunchArgs &a,
@@ -699,11 +711,7 @@ hipError_t launch_kernel(const void *fn, int64_t work_blocks, bool persistent, c
         if (blocks > cap)
             blocks = cap;
     }
-    // one-tile-per-block grids stay within the 32-bit grid limit
-    if (blocks > 0x7fffffff)
-        blocks = 0x7fffffff;
-    if (blocks < 1)
-        blocks = 1;
+    blocks = clamp_grid(blocks, kBlock);
     void *args[] = {const_cast<LaunchArgs *>(&a)};
     return hipLaunchKernel(fn, dim3(static_cast<unsigned>(blocks)), dim3(kBlock), args,
                            static_cast<size_t>(lds_bytes), stream);
@@ -722,6 +730,9 @@ hipError_t launch_vector(const LaunchArgs &a, hipStream_t stream)
         const int64_t n_tiles = n_groups / (static_cast<int64_t>(kBlock) * U);
         const int64_t c = xcd_chunk(n_tiles);
         blocks = kXcds * ceil_div(ceil_div(n_tiles, c), kXcds) * c;
+        // this tile order is not grid-stride: a clamped grid would skip tiles
+        if (blocks != clamp_grid(blocks, kBlock))
+            return hipErrorInvalidConfiguration;
     }
 #endif
     // bytes of loads one lane keeps in flight: 4 elements of each
@@ -790,10 +801,7 @@ hipError_t launch_quantize(const QuantizeArgs &q, bool vector_path, hipStream_t 
                                    : reinterpret_cast<const void *>(&quantize_element_kernel<kGradF32>);
         blocks = ceil_div(q.n, kQuantBlock);
     }
-    if (blocks > 0x7fffffff)
-        blocks = 0x7fffffff;   // the kernels are grid-stride
-    if (blocks < 1)
-        blocks = 1;
+    blocks = clamp_grid(blocks, kQuantBlock);
     void *args[] = {const_cast<QuantizeArgs *>(&q)};
     return hipLaunchKernel(fn, dim3(static_cast<unsigned>(blocks)), dim3(kQuantBlock), args, 0,
                            stream);

@@ -27,7 +27,8 @@ __global__ __launch_bounds__(kBlock) void copy16(const f32x4 *__restrict__ src,
 }  // namespace
 
 // Copies `bytes` bytes (a multiple of 16, both pointers 16-byte aligned,
-// regions not overlapping, bytes / 16 < 2^31 * 64) from src to dst on
+// regions not overlapping, bytes / 16 < 2^32: one lane per 16 bytes, and a
+// dispatch counts its lanes in 32 bits) from src to dst on
 // `stream`.  Returns 0, or -1 for bad arguments (nothing launched), or the
 // HIP error code of the launch.
 extern "C" int disdp_probe_copy(const void *src, void *dst, int64_t bytes, hipStream_t stream)
@@ -37,7 +38,7 @@ extern "C" int disdp_probe_copy(const void *src, void *dst, int64_t bytes, hipSt
         return -1;
     const int64_t n16 = bytes / 16;
     const int64_t blocks = (n16 + kBlock - 1) / kBlock;
-    if (blocks > 0x7fffffff)
+    if (blocks * kBlock > 0xffffffffLL)
         return -1;
     const uintptr_t s = reinterpret_cast<uintptr_t>(src), d = reinterpret_cast<uintptr_t>(dst);
     if (s < d + static_cast<uintptr_t>(bytes) && d < s + static_cast<uintptr_t>(bytes))

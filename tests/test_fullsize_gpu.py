@@ -141,3 +141,54 @@ def test_full_size_trajectory_of_40_steps():
     finally:
         del dp, dm, dv, sh
         t_.cuda.empty_cache()
+
+
+def test_grids_beyond_2_to_the_32_lanes():
+    """A shard of 2^34 + 12,345 elements needs more one-tile blocks (and
+    more quantize lanes) than one dispatch counts (2^32 - 1 work-items):
+    the library clamps its grids and the kernels walk the rest grid-stride.
+    disdp_aggregate of one bf16 contribution in fp32 mode returns every
+    element widened, checked over all of them (arbitrary bit patterns, NaNs
+    included: no arithmetic touches them); disdp_quantize of the same array
+    matches the oracle on sampled elements, including those the clamped grid
+    reaches on its second pass and the last ones."""
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    n = (1 << 34) + 12_345
+    free, _ = t_.cuda.mem_get_info()
+    if n * 6 + (1 << 31) > 0.92 * free:
+        pytest.skip(f"needs {n * 6 / 2**30:.0f} GiB, {free / 2**30:.0f} free")
+    chunk = 1 << 28
+    print(f"[fullsize] 2^34+ n={n} fill", flush=True)
+    g = t_.empty(n, dtype=t_.int16, device="cuda")
+    gen = t_.Generator(device="cuda")
+    gen.manual_seed(34)
+    for s in range(0, n, chunk):
+        e = min(n, s + chunk)
+        g[s:e] = t_.randint(-32768, 32768, (e - s,), dtype=t_.int32, device="cuda",
+                            generator=gen).to(t_.int16)
+    agg = t_.empty(n, dtype=t_.float32, device="cuda")
+    print("[fullsize] 2^34+ aggregate", flush=True)
+    dd.aggregate([g], mode="fp32", agg_out_f32=agg)
+    t_.cuda.synchronize()
+    for s in range(0, n, chunk):
+        e = min(n, s + chunk)
+        same = t_.equal(agg[s:e].view(t_.int32), g[s:e].to(t_.int32) << 16)
+        assert same, f"aggregate differs in [{s}, {e})"
+    del agg
+    out = t_.empty(n, dtype=t_.int32, device="cuda")
+    print("[fullsize] 2^34+ quantize", flush=True)
+    dd.quantize(g, out, frac_bits=24)
+    t_.cuda.synchronize()
+    # one 64-lane block per 256 elements, at most (2^32 - 1) // 64 blocks:
+    # the first pass of the clamped grid ends here
+    first_pass = ((2**32 - 1) // 64) * 64 * 4
+    idx = np.unique(np.concatenate([sample_indices(n, 34),
+                                    np.arange(first_pass - 300, first_pass + 300)]))
+    ti = t_.from_numpy(idx).cuda()
+    gh = g[ti].cpu().numpy().view(np.uint16)
+    want = oracle.quantize_array(gh, 24)
+    got = out[ti].cpu().numpy()
+    assert np.array_equal(got, want)
+    del out, g
+    t_.cuda.empty_cache()
