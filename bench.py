@@ -14,6 +14,7 @@ lr 1e-4, betas (0.9, 0.95), eps 1e-8, weight decay 0.1.
     python bench.py --interference      # fused call next to a bf16 GEMM loop
     python bench.py --copy-probe        # plain 4 GiB device copy (counter scale)
     python bench.py --entry aggregate   # another entry point on the same shard
+    python bench.py --entry fused_graph # the fused call replayed as one HIP graph
 
 Prints one JSON line.  ``roofline`` prices the kernel against HBM bandwidth
 (8 TB/s) with algorithmic bytes (each byte the call must move, counted once);
@@ -452,8 +453,6 @@ def run_entry(args):
     gb = 2 if wl.gdtype == "bf16" else 4
     kw = dict(lr=hp["lr"], beta1=hp["beta1"], beta2=hp["beta2"], eps=hp["eps"],
               weight_decay=hp["wd"])
-    graph = None
-
     def prepare(t):
         pass
 

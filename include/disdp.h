@@ -55,9 +55,17 @@
  *             vector kernels run when every array starts the same number of
  *             elements past a 4-element boundary (16 bytes for 4-byte
  *             arrays, 8 for bf16), e.g. any sub-range of aligned arrays: the
- *             first few elements (up to 63, reaching a common 64-element
- *             boundary when the arrays agree that far) are done one by one.
- *             Otherwise an element-wise kernel runs.
+ *             first few elements (up to 255, reaching a common 256- or
+ *             64-element boundary when the arrays agree that far) are done
+ *             one by one.
+ *             Arrays with unrelated offsets take them too when every array
+ *             is aligned to its element size and the bf16 arrays can reach
+ *             4-byte boundaries together: the first output is brought to a
+ *             256-element boundary (or one element past it) and the others
+ *             are read and written at 4-byte-aligned addresses.  Otherwise
+ *             (an array not aligned to its element size, or bf16 arrays at
+ *             both odd and even element offsets) an element-wise kernel
+ *             runs.
  * Errors      Arguments are checked on the host in this order: counts and
  *             enumerations, hyperparameters, then (only when n > 0) NULL
  *             pointers, overlap, and -- the first HIP call -- that every

@@ -115,43 +115,87 @@ bool gpu_addressable(const void *p)
     }
 }
 
+// A vector kernel's tile is 256 elements (a one-wave block of 64 lanes x 4
+// elements): 1 KiB of every 4-byte array.  Tiles that start on a 1 KiB
+// boundary stream about 5% faster on MI355X than tiles straddling two
+// (measured with every array offset by 64, 128 or 192 elements against 0,
+// 256 or 512), so the head reaches a 256-element boundary when it can.
+constexpr int kTileElems = 256;
+
 // Elements to do one by one before the vector kernels can take arrays
-// `p[0..np)` of element sizes `esz`: 0 when all are aligned to 64 elements
-// (or to 4 elements but not all to 64), the distance to the next common
-// 64- or 4-element boundary when they share a phase, -1 when they do not
-// (or an array is not aligned to its own element size).  Never more than n.
+// `p[0..np)` of element sizes `esz` that share a phase: the distance to the
+// next common 256-, 64- or 4-element boundary (the coarsest they share),
+// -1 when they share none or an array is not aligned to its own element
+// size.  Never more than n.
 int common_head(const void *const *p, const int *esz, int np, int64_t n)
 {
-    int ph64 = -1;
-    bool same64 = true, same4 = true;
-    int ph4 = -1;
+    if (np == 0)
+        return 0;
+    int ph = -1;
+    bool same256 = true, same64 = true, same4 = true;
     for (int i = 0; i < np; ++i) {
         const uintptr_t u = reinterpret_cast<uintptr_t>(p[i]);
         if (u % esz[i])
             return -1;
-        const int e = static_cast<int>((u / esz[i]) & 63);
-        if (ph64 < 0) {
-            ph64 = e;
-            ph4 = e & 3;
-        }
-        same64 = same64 && e == ph64;
-        same4 = same4 && (e & 3) == ph4;
+        const int e = static_cast<int>((u / esz[i]) % kTileElems);
+        if (ph < 0)
+            ph = e;
+        same256 = same256 && e == ph;
+        same64 = same64 && (e & 63) == (ph & 63);
+        same4 = same4 && (e & 3) == (ph & 3);
     }
-    if (np == 0)
-        return 0;
     int64_t head;
-    if (same64)
-        head = (64 - ph64) & 63;
+    if (same256)
+        head = (kTileElems - ph) % kTileElems;
+    else if (same64)
+        head = (64 - (ph & 63)) & 63;
     else if (same4)
-        head = (4 - ph4) & 3;
+        head = (4 - (ph & 3)) & 3;
     else
         return -1;
     return static_cast<int>(head < n ? head : n);
 }
 
-// Shared body of the three entry points.  `adam` selects the optimizer;
-// for disdp_adam_step the single contribution is the fp32 aggregate itself
-// (an aggregate of one fp32 contribution is that contribution, unrounded).
+// Elements to do one by one before the vector kernels can take arrays that
+// share no phase (common_head found none): the reference array `p[ref]` (the
+// first output) is brought to a 256-element boundary, or to one element past
+// it when that puts every 2-byte array on a 4-byte boundary, and every other
+// array is then accessed at whatever 4-byte-aligned address it has (a group
+// access needs 4-byte alignment only).  -1 when no head does that (2-byte
+// arrays at both odd and even element offsets) or an array is not aligned
+// to its element size.  Never more than n.
+int shifted_head(const void *const *p, const int *esz, int np, int ref, int64_t n)
+{
+    for (int i = 0; i < np; ++i)
+        if (reinterpret_cast<uintptr_t>(p[i]) % esz[i])
+            return -1;
+    const uintptr_t r = reinterpret_cast<uintptr_t>(p[ref]) / esz[ref];
+    int head = static_cast<int>((kTileElems - r % kTileElems) % kTileElems);
+    for (int attempt = 0; attempt < 2; ++attempt, head = (head + 1) % kTileElems) {
+        bool ok = true;
+        for (int i = 0; i < np && ok; ++i)
+            ok = (reinterpret_cast<uintptr_t>(p[i]) +
+                  static_cast<uintptr_t>(head) * static_cast<uintptr_t>(esz[i])) % 4 == 0;
+        if (ok)
+            return static_cast<int>(head < n ? head : n);
+    }
+    return -1;
+}
+
+// The head of a launch over arrays p[0..np), the first output at p[ref]:
+// the common phase when the arrays share one, else the shifted head, else
+// -1 (the element-wise kernel).
+int vector_head(const void *const *p, const int *esz, int np, int ref, int64_t n)
+{
+    const int head = common_head(p, esz, np, n);
+    return head >= 0 || ref >= np ? head : shifted_head(p, esz, np, ref, n);
+}
+
+// Shared body of the aggregation and optimizer entry points.  `adam`
+// selects the optimizer; for disdp_adam_step the single contribution is the
+// fp32 aggregate itself (an aggregate of one fp32 contribution is that
+// contribution, unrounded).  With `scalars_in_memory` the step constants
+// are not derived from `hp` but read by the kernel from `s_dev`.
 disdp_status_t run(const void *const *grads, int W, int gdtype, int64_t n,
                    int mode, int frac_bits, float *param, float *m, float *v,
                    uint16_t *p16, float *agg_f32, int32_t *agg_i32,
@@ -243,10 +287,12 @@ disdp_status_t run(const void *const *grads, int W, int gdtype, int64_t n,
     // arrays, 8-byte groups of 2-byte arrays.  Arrays that all start the same
     // number of elements past such a boundary (a sub-range of aligned arrays)
     // take the vector kernel too: their first elements are done one by one
-    // and the pointers advanced.  When the arrays agree modulo 64 elements
-    // the pointers are advanced to a 64-element boundary, which starts every
-    // array on a whole cache line (256 B for 4-byte arrays, 128 B for 2-byte
-    // ones): a wave's stores then cover whole lines, as for aligned arrays.
+    // and the pointers advanced.  When the arrays agree modulo 256 (or 64)
+    // elements the pointers are advanced to such a boundary, which starts
+    // every tile on a 1 KiB boundary (or at least every wave's stores on
+    // whole cache lines), as for aligned arrays.  Arrays with unrelated
+    // offsets put the first output on a tile boundary and the others
+    // wherever they fall on 4-byte boundaries.
     const void *ptrs[disdp::kMaxW + 6];
     int sizes[disdp::kMaxW + 6];
     int np = 0;
@@ -261,7 +307,7 @@ disdp_status_t run(const void *const *grads, int W, int gdtype, int64_t n,
             ptrs[np] = outs_p[k];
             sizes[np++] = outs_sz[k];
         }
-    const int head = common_head(ptrs, sizes, np, n);
+    const int head = vector_head(ptrs, sizes, np, /*ref=*/W, n);
     const bool vec = head >= 0;
     if (head > 0) {
         a.head = head;
@@ -370,11 +416,11 @@ disdp_status_t disdp_quantize(const void *grad, disdp_dtype_t gdtype, int64_t n,
     q.head = 0;
     q.gdtype = gdtype;
     q.qscale = std::ldexp(1.0f, frac_bits);
-    // as in run(): a common misalignment is peeled off one element at a time
+    // as in run(): a misalignment is peeled off one element at a time
     const int gb = grad_bytes(gdtype);
     const void *ptrs[2] = {grad, out};
     const int sizes[2] = {gb, 4};
-    const int head = common_head(ptrs, sizes, 2, n);
+    const int head = vector_head(ptrs, sizes, 2, /*ref=*/1, n);
     const bool vec = head >= 0;
     if (head > 0) {
         q.head = head;

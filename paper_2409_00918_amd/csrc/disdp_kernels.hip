@@ -129,35 +129,42 @@ namespace {
 
 constexpr int kBlock = DISDP_BLOCK;
 constexpr int kQuantBlock = DISDP_QUANT_BLOCK;
-// block 0 does up to 63 head elements and 3 tail elements, one per lane
+// block 0 does the head elements (a loop over its lanes) and the 3 tail
+// elements (one per lane)
 static_assert(DISDP_BLOCK % 64 == 0 && DISDP_QUANT_BLOCK % 64 == 0,
               "blocks are whole 64-lane waves");
 constexpr int kWave = 64;
 
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+// Vector types of the 4-element groups, declared only 4-byte aligned: a
+// group of an array that starts off its natural vector boundary (arrays with
+// unrelated misalignments) is one 16- or 8-byte access at a 4-byte-aligned
+// address, which the global memory instructions take as they are (for
+// naturally aligned groups the machine code is the same).
+typedef float f32x4 __attribute__((ext_vector_type(4), aligned(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2), aligned(4)));
+typedef int32_t i32x4 __attribute__((ext_vector_type(4), aligned(4)));
 
-template <typename T>
-__device__ __forceinline__ T ld_nt(const T *p)
-{
-#if DISDP_NT & 1
-    return __builtin_nontemporal_load(p);
-#else
-    return *p;
-#endif
-}
-
-template <typename T>
-__device__ __forceinline__ void st_nt(T *p, T v)
-{
-#if DISDP_NT & 2
-    __builtin_nontemporal_store(v, p);
-#else
-    *p = v;
-#endif
-}
+// Non-temporal group loads and stores.  Overloads, not a template: deducing
+// the vector type would drop the typedef's 4-byte alignment.
+#define DISDP_NT_ACCESS(T)                                  \
+    __device__ __forceinline__ T ld_nt(const T *p)          \
+    {                                                       \
+        if constexpr (DISDP_NT & 1)                         \
+            return __builtin_nontemporal_load(p);           \
+        else                                                \
+            return *p;                                      \
+    }                                                       \
+    __device__ __forceinline__ void st_nt(T *p, T v)        \
+    {                                                       \
+        if constexpr (DISDP_NT & 2)                         \
+            __builtin_nontemporal_store(v, p);              \
+        else                                                \
+            *p = v;                                         \
+    }
+DISDP_NT_ACCESS(f32x4)
+DISDP_NT_ACCESS(u32x2)
+DISDP_NT_ACCESS(i32x4)
+#undef DISDP_NT_ACCESS
 
 // ---- element operations ---------------------------------------------------
 
@@ -509,8 +516,9 @@ __global__ DISDP_LAUNCH_BOUNDS void vector_kernel(LaunchArgs a)
     if (blockIdx.x == 0 && threadIdx.x < (a.n & 3))
         process_element<GT, MODE, ADAM>(a, (n_groups << 2) + threadIdx.x);
     // the elements before the vector-aligned pointers
-    if (blockIdx.x == 0 && threadIdx.x < a.head)
-        process_element<GT, MODE, ADAM>(a, static_cast<int64_t>(threadIdx.x) - a.head);
+    if (blockIdx.x == 0)
+        for (int j = threadIdx.x; j < a.head; j += kBlock)
+            process_element<GT, MODE, ADAM>(a, static_cast<int64_t>(j) - a.head);
 }
 
 // Element-wise kernel for buffers that are not vector aligned.
@@ -544,10 +552,11 @@ __global__ DISDP_QUANT_LAUNCH_BOUNDS void quantize_vector_kernel(QuantizeArgs q)
         const int64_t i = (n_groups << 2) + threadIdx.x;
         q.out[i] = quantize(load_one<GT>(q.g, i), q.qscale);
     }
-    if (blockIdx.x == 0 && threadIdx.x < q.head) {
-        const int64_t i = static_cast<int64_t>(threadIdx.x) - q.head;
-        q.out[i] = quantize(load_one<GT>(q.g, i), q.qscale);
-    }
+    if (blockIdx.x == 0)
+        for (int j = threadIdx.x; j < q.head; j += kQuantBlock) {
+            const int64_t i = static_cast<int64_t>(j) - q.head;
+            q.out[i] = quantize(load_one<GT>(q.g, i), q.qscale);
+        }
 }
 
 template <int GT>

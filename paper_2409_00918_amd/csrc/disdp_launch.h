@@ -30,7 +30,7 @@ struct LaunchArgs {
     float *agg_f32;        // optional fp32 aggregate
     int32_t *agg_i32;      // optional int32 aggregate (fixed mode)
     int64_t n;             // elements from the pointers on
-    int head;              // 0-63 elements just before the pointers, done one
+    int head;              // 0-255 elements just before the pointers, done one
                            // by one (pointers advanced to vector alignment)
     int W, gdtype, mode, frac_bits;
     float qscale, dqscale; // 2^k and 2^-k (fixed mode)

@@ -11,7 +11,8 @@
 //     fused calls: the step constants passed by value, or by address only);
 //   * valid calls whose arrays share, or do not share, a misalignment: the
 //     vector/element choice, the head of elements done one by one and the
-//     advanced pointers.
+//     advanced pointers (on a common boundary, or every array on a 4-byte
+//     boundary with the first output on a 64-element one).
 //
 // Prints "api_fuzz: ok" and exits 0; any failed check prints the case and
 // exits 1; a sanitizer finding aborts.
@@ -399,13 +400,15 @@ void fuzz_alignment(int iters)
         // disturbed: a different phase mod 64 but the same mod 4, a different
         // phase mod 4, or an address not a multiple of the element size
         const int phase = static_cast<int>(below(64));
-        const int disturb = static_cast<int>(below(4));
+        const int disturb = static_cast<int>(below(5));
         const int victim = static_cast<int>(below(W + 4));
         int extra = 0;
         if (disturb == 1)
             extra = 4 * (1 + static_cast<int>(below(15)));
         else if (disturb == 2)
             extra = 1 + static_cast<int>(below(3));
+        else if (disturb == 4)
+            extra = 64 * (1 + static_cast<int>(below(3)));
         const void *g[disdp::kMaxW];
         for (int w = 0; w < W; ++w)
             g[w] = fake(w) + int64_t(gb) * (phase + (victim == w ? extra : 0)) +
@@ -424,11 +427,32 @@ void fuzz_alignment(int iters)
                                                        nullptr, &hp, nullptr);
         CHECK(st == DISDP_OK, "status %d", st);
         const disdp::LaunchArgs &a = g_args;
-        // disturb 0: one shared phase mod 64 -> head to the 64-element
-        // boundary; 1: same phase mod 4 only -> head to the 4-element one;
-        // 2, 3: no shared phase or a misaligned element -> element kernel
-        bool want_vec = disturb <= 1;
-        int64_t want_head = disturb == 0 ? (64 - phase) & 63 : disturb == 1 ? (4 - (phase & 3)) & 3 : 0;
+        // disturb 0: one shared phase mod 256 -> head to the 256-element
+        // boundary; 4: same phase mod 64 only -> head to the 64-element one;
+        // 1: same phase mod 4 only -> head to the 4-element one;
+        // 2: no shared phase -> head taking p to a 256-element boundary, or
+        // one element past it, such that every 2-byte array lands on a 4-byte
+        // boundary (the fake bases are multiples of 4), else element kernel;
+        // 3: an element not aligned to its size -> element kernel
+        auto ph = [&](int idx) { return phase + (victim == idx ? extra : 0); };
+        bool want_vec = disturb <= 1 || disturb == 4;
+        int64_t want_head = disturb == 0   ? (256 - phase) % 256
+                            : disturb == 4 ? (64 - phase) & 63
+                            : disturb == 1 ? (4 - (phase & 3)) & 3
+                                           : 0;
+        if (disturb == 2) {
+            const int h0 = (256 - ph(W) % 256) % 256;
+            for (int h : {h0, (h0 + 1) % 256}) {
+                bool ok = (ph(W + 3) + h) % 2 == 0;           // the bf16 copy
+                for (int w = 0; w < W && gb == 2; ++w)
+                    ok = ok && (ph(w) + h) % 2 == 0;          // bf16 contributions
+                if (ok) {
+                    want_vec = true;
+                    want_head = h;
+                    break;
+                }
+            }
+        }
         if (want_head > n)
             want_head = n;
         CHECK(g_vec == want_vec, "vec %d want %d (disturb %d phase %d)", g_vec, want_vec, disturb,
@@ -442,8 +466,18 @@ void fuzz_alignment(int iters)
         for (int w = 0; w < W; ++w)
             CHECK(a.g[w] == static_cast<const char *>(g[w]) + int64_t(a.head) * gb,
                   "contribution %d not advanced by the head", w);
-        if (g_vec && a.n > 0) {
-            const int gran = disturb == 0 ? 64 : 4;
+        if (g_vec && a.n > 0 && disturb == 2) {
+            const uintptr_t pe = reinterpret_cast<uintptr_t>(a.p) / 4 % 256;
+            CHECK(pe == 0 || pe == 1, "p at element %d past a 256-element boundary",
+                  static_cast<int>(pe));
+            const void *all[] = {a.p, a.m, a.v, a.p16};
+            for (const void *q : all)
+                CHECK(reinterpret_cast<uintptr_t>(q) % 4 == 0, "state not on a 4-byte boundary");
+            for (int w = 0; w < W; ++w)
+                CHECK(reinterpret_cast<uintptr_t>(a.g[w]) % 4 == 0,
+                      "contribution %d not on a 4-byte boundary", w);
+        } else if (g_vec && a.n > 0) {
+            const int gran = disturb == 0 ? 256 : disturb == 4 ? 64 : 4;
             for (int w = 0; w < W; ++w)
                 CHECK((reinterpret_cast<uintptr_t>(a.g[w]) / gb) % gran == 0,
                       "contribution %d not on a %d-element boundary", w, gran);

@@ -64,20 +64,112 @@ def test_fused_unaligned_pointers(offsets, gdtype, mode):
         assert_parity(got, want, _label(offsets=offsets, n=n))
 
 
-@pytest.mark.parametrize("k", [1, 2, 3, 37, 63])
+@pytest.mark.parametrize("k", [1, 2, 3, 37, 63, 64, 130, 200, 255])
 @pytest.mark.parametrize("gdtype,mode", [("f32", "fp32"), ("bf16", "fixed"), ("bf16", "fp32"),
                                          ("f32", "fixed")])
 def test_fused_common_misalignment(k, gdtype, mode):
-    """Every array starts k elements past a 64-element boundary (a sub-range
-    of aligned arrays): the library does the first 64 - k elements one by one
-    and runs the vector kernel on the rest.  Lengths shorter than that head
-    included."""
-    for n in (1, 2, 3, 4, 5, 26, 27, 28, 63, 64, 65, 1027, 40_001, 262_147):
+    """Every array starts k elements past a 256-element boundary (a sub-range
+    of aligned arrays): the library does the first 256 - k elements one by
+    one (block 0 looping over its lanes) and runs the vector kernel on the
+    rest.  Lengths shorter than that head included."""
+    for n in (1, 2, 3, 4, 5, 26, 27, 28, 63, 64, 65, 125, 126, 127, 192, 193, 255, 256, 257,
+              1027, 40_001, 262_147):
         got, want = run_fused_case(8, gdtype, mode, n, t=3, offsets=(k, k), seed=11 + k)
         assert_parity(got, want, _label(k=k, gdtype=gdtype, mode=mode, n=n))
 
 
-@pytest.mark.parametrize("k", [1, 2, 3, 50])
+def _offsets(rng, count, two_byte, even):
+    """Element offsets in [0, 64) for `count` arrays; with `even`, the
+    2-byte arrays (flags in `two_byte`) all get even offsets."""
+    o = [int(x) for x in rng.integers(0, 64, count)]
+    if even:
+        o = [x & ~1 if tb else x for x, tb in zip(o, two_byte)]
+    return o
+
+
+@pytest.mark.parametrize("gdtype,mode", [("f32", "fp32"), ("bf16", "fp32"), ("f32", "fixed"),
+                                         ("bf16", "fixed")])
+def test_fused_unrelated_misalignments(gdtype, mode):
+    """Every array at its own element offset: the vector kernels with the
+    first output on a 64-element boundary and the other arrays at
+    4-byte-aligned addresses (bf16 arrays at offsets of one parity), or the
+    element kernel (bf16 arrays of both parities).  Against the oracle over
+    lengths from below one group to many tiles with a ragged tail."""
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    rng = np.random.default_rng(77 if gdtype == "f32" else 78)
+    cases = [(1, 1), (3, 5), (8, 63), (8, 64), (5, 1027), (16, 40_001), (8, 262_147), (9, 70_001)]
+    for i, (W, n) in enumerate(cases):
+        for even in (True, False):
+            bf = gdtype == "bf16"
+            # contributions, p, m, v, bf16 copy, fp32 aggregate, int32 aggregate
+            two = [bf] * W + [False, False, False, True, False, False]
+            o = _offsets(rng, W + 6, two, even)
+            gs = synth.host_grads(700 + i, 1, W, n, 1e-4, gdtype=gdtype,
+                                  outlier_frac=0.01, outlier_scale=100.0)
+            p, m, v = synth.host_state(700 + i, n, mv_sigma=1e-4)
+            dg = [to_dev(g, o[w]) for w, g in enumerate(gs)]
+            dp, dm, dv = to_dev(p, o[W]), to_dev(m, o[W + 1]), to_dev(v, o[W + 2])
+            d16 = to_dev(np.zeros(n, np.uint16), o[W + 3])
+            daf = to_dev(np.zeros(n, np.float32), o[W + 4])
+            dai = to_dev(np.zeros(n, np.int32), o[W + 5]) if mode == "fixed" else None
+            dd.aggregate_adam(dg, dp, dm, dv, d16, lr=HP["lr"], beta1=HP["beta1"],
+                              beta2=HP["beta2"], eps=HP["eps"], weight_decay=HP["wd"],
+                              step=2, mode=mode, frac_bits=24, agg_out_f32=daf,
+                              agg_out_i32=dai)
+            t_.cuda.synchronize()
+            want = oracle.fused(gs, p, m, v, mode=oracle.AGG_FIXED if mode == "fixed"
+                                else oracle.AGG_FP32, frac_bits=24, t=2,
+                                want_agg_f32=True, want_agg_i32=mode == "fixed", **HP)
+            got = {"p": to_host(dp), "m": to_host(dm), "v": to_host(dv),
+                   "p16": to_host(d16), "agg_f32": to_host(daf)}
+            if dai is not None:
+                got["agg_i32"] = to_host(dai)
+            assert_parity(got, want, _label(W=W, n=n, offsets=o))
+
+
+def test_aggregate_adam_step_and_quantize_unrelated_misalignments():
+    """The same for the single-purpose calls: disdp_aggregate (the first
+    output is the fp32 or the int32 aggregate), disdp_adam_step and
+    disdp_quantize, each array at its own offset."""
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    rng = np.random.default_rng(79)
+    for i, n in enumerate([2, 255, 4099, 70_001]):
+        for gdtype in ("f32", "bf16"):
+            W = 5
+            two = [gdtype == "bf16"] * W + [False, False]
+            o = _offsets(rng, W + 2, two, True)
+            gs = synth.host_grads(720 + i, 1, W, n, 1e-4, gdtype=gdtype,
+                                  outlier_frac=0.01, outlier_scale=100.0)
+            dg = [to_dev(g, o[w]) for w, g in enumerate(gs)]
+            ai = to_dev(np.zeros(n, np.int32), o[W])
+            af = to_dev(np.zeros(n, np.float32), o[W + 1])
+            dd.aggregate(dg, mode="fixed", frac_bits=24, agg_out_i32=ai)
+            dd.aggregate(dg, mode="fp32", agg_out_f32=af)
+            t_.cuda.synchronize()
+            lab = _label(n=n, gdtype=gdtype, offsets=o)
+            assert np.array_equal(to_host(ai), oracle.aggregate_fixed(gs, 24)[0]), lab
+            assert f32_same(to_host(af), oracle.aggregate_f32(gs)), lab
+            q = to_dev(np.zeros(n, np.int32), (o[0] + 7) % 64)
+            dd.quantize(dg[1], q, frac_bits=20)
+            t_.cuda.synchronize()
+            assert np.array_equal(to_host(q), oracle.quantize_array(gs[1], 20)), lab
+        p, m, v = synth.host_state(730 + i, n, mv_sigma=1e-4)
+        o = _offsets(rng, 5, [False, False, False, False, True], True)
+        agg = oracle.aggregate_f32(synth.host_grads(731 + i, 1, 2, n, 1e-4))
+        dagg = to_dev(agg, o[0])
+        dp, dm, dv = to_dev(p, o[1]), to_dev(m, o[2]), to_dev(v, o[3])
+        d16 = to_dev(np.zeros(n, np.uint16), o[4])
+        dd.adam_step(dagg, dp, dm, dv, d16, lr=HP["lr"], beta1=HP["beta1"], beta2=HP["beta2"],
+                     eps=HP["eps"], weight_decay=HP["wd"], step=3)
+        t_.cuda.synchronize()
+        p1, m1, v1, p16 = oracle.adamw(agg, p, m, v, t=3, **HP)
+        assert_parity({"p": to_host(dp), "m": to_host(dm), "v": to_host(dv), "p16": to_host(d16)},
+                      {"p": p1, "m": m1, "v": v1, "p16": p16}, f"adam_step n={n} offsets={o}")
+
+
+@pytest.mark.parametrize("k", [1, 2, 3, 50, 130])
 def test_aggregate_and_adam_step_common_misalignment(k):
     import paper_2409_00918_amd as dd
     t_ = torch()
@@ -699,8 +791,8 @@ def test_quantize_matches_oracle(gdtype, k):
                              outlier_scale=1e6)[0]
         if gdtype == "f32" and n > 8:
             g[:6] = np.array([np.inf, -np.inf, np.nan, 3e38, -3e38, 1e-45], np.float32)
-        for off in ((0, 0), (1, 3), (1, 1), (2, 2), (3, 3), (5, 1), (45, 45)) if n > 4 \
-                else ((0, 0), (2, 2), (45, 45)):
+        for off in ((0, 0), (1, 3), (1, 1), (2, 2), (3, 3), (5, 1), (45, 45), (200, 200),
+                    (7, 130)) if n > 4 else ((0, 0), (2, 2), (45, 45), (200, 200)):
             out = to_dev(np.zeros(n, np.int32), off[1])
             dd.quantize(to_dev(g, off[0]), out, frac_bits=k)
             t_.cuda.synchronize()
