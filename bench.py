@@ -319,6 +319,8 @@ def run_bench(args):
                    "frac_bits": wl.frac_bits, "optimizer": "AdamW",
                    "lr": wl.lr, "betas": [wl.beta1, wl.beta2], "eps": wl.eps,
                    "weight_decay": wl.wd, "bf16_copy": True,
+                   "shard_memory": ("one physically contiguous allocation" if sh.contiguous
+                                    else "one allocation (caching allocator)"),
                    "parallelism": "single GPU, one shard"},
         "roofline": roofline,
         "cpu_baseline": base,

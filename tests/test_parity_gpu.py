@@ -987,3 +987,39 @@ def test_fused_on_a_shard_placed_by_the_layout_planner(W, gdtype, mode):
     if mode == "fixed":
         got["agg_i32"] = to_host(sh.agg_i32)
     assert_parity(got, want, f"shard W={W} {gdtype} {mode}")
+
+
+def test_contiguous_shard_slab_lifetime():
+    """allocate_shard's physically contiguous slab: every view sits at the
+    planner's offset inside it, the memory stays valid while any view is
+    alive after the Shard object is gone, and is returned to the device when
+    the last view goes."""
+    import gc
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    n, W = 50_000_000, 4
+    gc.collect()
+    t_.cuda.synchronize()
+    free0, _ = t_.cuda.mem_get_info()
+    sh = dd.allocate_shard(n, W, "f32")
+    assert sh.contiguous, "the runtime refused a physically contiguous slab"
+    offs, total = dd.shard_layout(n, W, "f32")
+    base = sh.slab.data_ptr()
+    for i, x in enumerate(sh.grads + [sh.param, sh.m, sh.v, sh.param_bf16]):
+        assert x.data_ptr() == base + offs[i], i
+    slack = 64 << 20                 # device-wide free-memory accounting is not exact
+    free1, _ = t_.cuda.mem_get_info()
+    assert free0 - free1 >= total - slack
+    keep = sh.v
+    keep.fill_(1.5)
+    del sh, x
+    gc.collect()
+    t_.cuda.synchronize()
+    free2, _ = t_.cuda.mem_get_info()
+    assert free0 - free2 >= total - slack         # still held by the view
+    assert bool((keep[-1000:] == 1.5).all()) and bool((keep[:1000] == 1.5).all())
+    del keep
+    gc.collect()
+    t_.cuda.synchronize()
+    free3, _ = t_.cuda.mem_get_info()
+    assert free0 - free3 < total // 2             # returned
