@@ -63,10 +63,9 @@
 //                     (W <= 2 fp32 contributions with the optimizer, the
 //                     optimizer step alone): fewer bytes per wave need more
 //                     waves.
-//   DISDP_WAVES_PER_CU_FIXED  the same for fixed-point mode, whose lanes
-//                     spend ~4x more instructions per element converting
-//                     contributions and so need more resident waves to keep
-//                     loads in flight.
+//   DISDP_WAVES_PER_CU_FIXED  when > 0, one cap for every fixed-point kernel
+//                     that converts float contributions; by default
+//                     (0) the cap comes from fixed_mode_waves() below.
 //                     The quantize kernel (one load per lane) is not capped.
 //   DISDP_XCD_CHUNK   0: block b takes tile b.  C > 0 (one tile per block):
 //                     the dispatcher deals blocks round-robin to the 8
@@ -102,7 +101,7 @@
 #define DISDP_WAVES_PER_CU 8
 #endif
 #ifndef DISDP_WAVES_PER_CU_FIXED
-#define DISDP_WAVES_PER_CU_FIXED 12
+#define DISDP_WAVES_PER_CU_FIXED 0
 #endif
 #ifndef DISDP_WAVES_PER_CU_SMALL
 #define DISDP_WAVES_PER_CU_SMALL 12
@@ -571,6 +570,23 @@ __global__ DISDP_QUANT_LAUNCH_BOUNDS void quantize_element_kernel(QuantizeArgs q
 
 constexpr int kU = DISDP_UNROLL;
 
+// Resident waves per CU for a fixed-point kernel converting float
+// contributions, whose lanes spend ~4x more instructions per element than
+// in fp32 mode and so hold loads in flight for a smaller share of the time.
+// The best cap falls with the bytes a lane keeps in flight and rises with
+// the conversions per byte (bf16 contributions have twice as many).
+// Interleaved A/B of the fused call at n = 4e8 over caps of 8-16 (TB/s at
+// the chosen cap vs the next best): fp32 W = 1, 2 (64, 80 B) 14; W = 4
+// (112 B) 12; W = 8 (176 B) 10, with 8 within 0.3%; W = 12, 16 (240,
+// 304 B) 8; bf16 W = 8, 16 14.  Int32 contributions need no conversion and
+// take the fp32-mode caps.
+constexpr int fixed_mode_waves(int lane_bytes, bool bf16)
+{
+    if (DISDP_WAVES_PER_CU_FIXED > 0)
+        return DISDP_WAVES_PER_CU_FIXED;
+    return bf16 || lane_bytes <= 80 ? 14 : lane_bytes <= 112 ? 12 : lane_bytes <= 176 ? 10 : 8;
+}
+
 // Dynamic LDS bytes a vector-kernel block reserves so that at most
 // `blocks_per_cu` blocks fit on a CU (0 = no cap), cached per device.
 int occupancy_lds_bytes(int blocks_per_cu)
@@ -643,8 +659,8 @@ int stream_cus(hipStream_t stream)
 // resident waves chip-wide, so on a stream restricted to fewer CUs each CU
 // takes proportionally more, up to kMaxScaledWaves (the register limit of
 // the W = 8 kernels).  Measured on the 7B/8 shard with 32 / 64 / 128 CUs:
-// 20 waves per CU streamed 41% / 35% / 19% faster than 12, which is best
-// on all 256.
+// 20 waves per CU streamed 41% / 35% / 19% faster than the full-chip cap
+// of the time (12 waves per CU, in 4-wave blocks).
 #ifndef DISDP_MAX_SCALED_WAVES
 #define DISDP_MAX_SCALED_WAVES 20
 #endif
@@ -745,10 +761,11 @@ hipError_t launch_vector(const LaunchArgs &a, hipStream_t stream)
     }
 #endif
     // bytes of loads one lane keeps in flight: 4 elements of each
-    // contribution, plus p, m and v with the optimizer
+    // contribution, plus p, m and v with the optimizer (run-time W: many)
     constexpr int kGradBytes = GT == kGradBF16 ? 2 : 4;
     constexpr int kLaneBytes = W > 0 ? 4 * (W * kGradBytes + (ADAM ? 12 : 0)) : 1 << 30;
-    constexpr int base = MODE == kAggFixed ? DISDP_WAVES_PER_CU_FIXED
+    constexpr bool kConverts = MODE == kAggFixed && GT != kGradI32;
+    constexpr int base = kConverts ? fixed_mode_waves(kLaneBytes, GT == kGradBF16)
                          : kLaneBytes <= DISDP_SMALL_LANE_BYTES ? DISDP_WAVES_PER_CU_SMALL
                                                                 : DISDP_WAVES_PER_CU;
     return launch_kernel(reinterpret_cast<const void *>(&vector_kernel<W, GT, MODE, ADAM, U>),
