@@ -50,19 +50,13 @@
 //   DISDP_WAVE_CONTIG 1: a wave's U groups are contiguous (U KiB per fp32
 //                     stream per wave); 0: strided by the block width
 //   DISDP_MIN_WAVES   launch-bounds hint: waves per SIMD to fit (0 = none)
-//   DISDP_WAVES_PER_CU  resident waves per CU for the fp32-mode fused and
-//                     aggregation vector kernels (0 = as many as registers
-//                     allow), enforced in whole blocks by reserving a share
-//                     of the CU's LDS per block (the kernels use no LDS).
-//                     With W + 3 16-byte loads in flight per lane, 8-12
-//                     waves (~135 KB in flight per CU) stream fastest: more
-//                     outstanding requests cost DRAM efficiency, 4 are too
-//                     few.
-//   DISDP_WAVES_PER_CU_SMALL  the cap for fp32-mode kernels whose lanes keep
-//                     at most DISDP_SMALL_LANE_BYTES of loads in flight
-//                     (W <= 2 fp32 contributions with the optimizer, the
-//                     optimizer step alone): fewer bytes per wave need more
-//                     waves.
+//   DISDP_WAVES_PER_CU  resident waves per CU for the fp32-mode vector
+//                     kernels (and int32 contributions), enforced in whole
+//                     blocks by reserving a share of the CU's LDS per block
+//                     (the kernels use no LDS): > 0 one cap for all, < 0 no
+//                     cap, 0 (default) the table of fp32_mode_waves() below.
+//                     Fewer waves than registers allow stream faster: more
+//                     outstanding requests cost DRAM efficiency.
 //   DISDP_WAVES_PER_CU_FIXED  when > 0, one cap for every fixed-point kernel
 //                     that converts float contributions; by default
 //                     (0) the cap comes from fixed_mode_waves() below.
@@ -98,16 +92,10 @@
 #define DISDP_MIN_WAVES 0
 #endif
 #ifndef DISDP_WAVES_PER_CU
-#define DISDP_WAVES_PER_CU 8
+#define DISDP_WAVES_PER_CU 0
 #endif
 #ifndef DISDP_WAVES_PER_CU_FIXED
 #define DISDP_WAVES_PER_CU_FIXED 0
-#endif
-#ifndef DISDP_WAVES_PER_CU_SMALL
-#define DISDP_WAVES_PER_CU_SMALL 12
-#endif
-#ifndef DISDP_SMALL_LANE_BYTES
-#define DISDP_SMALL_LANE_BYTES 80
 #endif
 #ifndef DISDP_XCD_CHUNK
 #define DISDP_XCD_CHUNK 0
@@ -389,12 +377,36 @@ __device__ __forceinline__ void process_groups(const LaunchArgs &a, int64_t g0, 
 
 // ---- one group per lane, W known only at run time (W <= 64) ---------------
 
-// Contributions are read in chunks of 8 (all 8 loads in flight, then the
-// eight additions in worker order).
+// K contributions w0 .. w0+K-1 into the accumulators: all K loads issued,
+// then the additions in worker order.  No branch separates the loads, so
+// none waits for the one before (a conditional load per contribution made
+// the compiler wait after each).  `first`: w0 is contribution 0.
+template <int K, int GT, int MODE>
+__device__ __forceinline__ void accumulate_piece(const LaunchArgs &a, int64_t grp, int w0,
+                                                 bool first, Acc<MODE> (&acc)[4])
+{
+    typename Contrib<GT>::type c[K][4];
+#pragma unroll
+    for (int j = 0; j < K; ++j)
+        load_group<GT>(a.g[w0 + j], grp, c[j]);
+#pragma unroll
+    for (int j = 0; j < K; ++j) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            if (j == 0 && first)
+                acc[e].first(c[j][e], a.qscale);
+            else
+                acc[e].next(c[j][e], a.qscale);
+        }
+    }
+}
+
+// Contributions in chunks of 128 bytes per lane (8 fp32 or int32, 16 bf16),
+// then the remaining W mod chunk in pieces of 8, 4, 2 and 1.
 template <int GT, int MODE, bool ADAM>
 __device__ __forceinline__ void process_group_rt(const LaunchArgs &a, int64_t grp)
 {
-    constexpr int kChunk = 8;
+    constexpr int kChunk = GT == kGradBF16 ? 16 : 8;
     f32x4 P{}, M{}, V{};
     if constexpr (ADAM) {
         P = ld_nt(reinterpret_cast<const f32x4 *>(a.p) + grp);
@@ -402,25 +414,26 @@ __device__ __forceinline__ void process_group_rt(const LaunchArgs &a, int64_t gr
         V = ld_nt(reinterpret_cast<const f32x4 *>(a.v) + grp);
     }
     Acc<MODE> acc[4];
-    for (int w0 = 0; w0 < a.W; w0 += kChunk) {
-        typename Contrib<GT>::type c[kChunk][4];
-#pragma unroll
-        for (int j = 0; j < kChunk; ++j)
-            if (w0 + j < a.W)
-                load_group<GT>(a.g[w0 + j], grp, c[j]);
-#pragma unroll
-        for (int j = 0; j < kChunk; ++j) {
-            if (w0 + j < a.W) {
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    if (w0 + j == 0)
-                        acc[e].first(c[j][e], a.qscale);
-                    else
-                        acc[e].next(c[j][e], a.qscale);
-                }
-            }
+    int w0 = 0;
+    for (; w0 + kChunk <= a.W; w0 += kChunk)
+        accumulate_piece<kChunk, GT, MODE>(a, grp, w0, w0 == 0, acc);
+    const int rest = a.W - w0;
+    if constexpr (kChunk > 8) {
+        if (rest & 8) {
+            accumulate_piece<8, GT, MODE>(a, grp, w0, w0 == 0, acc);
+            w0 += 8;
         }
     }
+    if (rest & 4) {
+        accumulate_piece<4, GT, MODE>(a, grp, w0, w0 == 0, acc);
+        w0 += 4;
+    }
+    if (rest & 2) {
+        accumulate_piece<2, GT, MODE>(a, grp, w0, w0 == 0, acc);
+        w0 += 2;
+    }
+    if (rest & 1)
+        accumulate_piece<1, GT, MODE>(a, grp, w0, w0 == 0, acc);
     float agg[4];
     int32_t ai[4];
 #pragma unroll
@@ -585,6 +598,38 @@ constexpr int fixed_mode_waves(int lane_bytes, bool bf16)
     if (DISDP_WAVES_PER_CU_FIXED > 0)
         return DISDP_WAVES_PER_CU_FIXED;
     return bf16 || lane_bytes <= 80 ? 14 : lane_bytes <= 112 ? 12 : lane_bytes <= 176 ? 10 : 8;
+}
+
+// Resident waves per CU in fp32 mode (and for int32 contributions), by the
+// bytes of loads a lane keeps in flight: fewer bytes per wave need more
+// waves to keep enough requests in flight, more bytes fewer.  Interleaved
+// A/B of the fused call at n = 4e8 over caps of 6-16: 12 waves for lanes up
+// to 112 B (fp32 W <= 4, bf16 W <= 8, the optimizer step alone), 8 up to
+// 176 B (fp32 W = 5-8, bf16 W = 12, 16), 6 beyond (fp32 W = 12, 16).
+constexpr int fp32_mode_waves(int lane_bytes)
+{
+    if (DISDP_WAVES_PER_CU != 0)
+        return DISDP_WAVES_PER_CU > 0 ? DISDP_WAVES_PER_CU : 0;
+    return lane_bytes <= 112 ? 12 : lane_bytes <= 176 ? 8 : 6;
+}
+
+// The same for the run-time worker-count kernel, from the actual W: whole
+// chunks keep 128 B per lane in flight (8 waves suffice), a remainder adds
+// round trips with fewer bytes (10, 12 in fixed mode), and W below one
+// chunk is all such pieces (14).  Measured for fp32 W = 9, 24, 64 and bf16
+// W = 13, 32, 64 in both modes.
+int runtime_w_waves(int W, int gt, int mode)
+{
+    const bool bf16 = gt == kGradBF16;
+    const int chunk = bf16 ? 16 : 8;
+    if (mode == kAggFixed && gt != kGradI32) {
+        if (DISDP_WAVES_PER_CU_FIXED > 0)
+            return DISDP_WAVES_PER_CU_FIXED;
+        return bf16 ? 14 : W % chunk ? 12 : 8;
+    }
+    if (DISDP_WAVES_PER_CU != 0)
+        return DISDP_WAVES_PER_CU > 0 ? DISDP_WAVES_PER_CU : 0;
+    return W < chunk ? 14 : W % chunk ? 10 : 8;
 }
 
 // Dynamic LDS bytes a vector-kernel block reserves so that at most
@@ -765,9 +810,9 @@ hipError_t launch_vector(const LaunchArgs &a, hipStream_t stream)
     constexpr int kGradBytes = GT == kGradBF16 ? 2 : 4;
     constexpr int kLaneBytes = W > 0 ? 4 * (W * kGradBytes + (ADAM ? 12 : 0)) : 1 << 30;
     constexpr bool kConverts = MODE == kAggFixed && GT != kGradI32;
-    constexpr int base = kConverts ? fixed_mode_waves(kLaneBytes, GT == kGradBF16)
-                         : kLaneBytes <= DISDP_SMALL_LANE_BYTES ? DISDP_WAVES_PER_CU_SMALL
-                                                                : DISDP_WAVES_PER_CU;
+    const int base = W == 0    ? runtime_w_waves(a.W, GT, MODE)
+                     : kConverts ? fixed_mode_waves(kLaneBytes, GT == kGradBF16)
+                                 : fp32_mode_waves(kLaneBytes);
     return launch_kernel(reinterpret_cast<const void *>(&vector_kernel<W, GT, MODE, ADAM, U>),
                          blocks, DISDP_GRID_MODE == 0, a, stream,
                          occupancy_lds_bytes(blocks_per_cu_cap(base, stream)));
