@@ -47,7 +47,9 @@ def test_fused_sweep_lengths(W, gdtype, mode):
         assert_parity(got, want, _label(W=W, gdtype=gdtype, mode=mode, n=n))
 
 
-@pytest.mark.parametrize("W", [5, 9, 13, 33, 64])
+# run-time worker counts: whole chunks (8 fp32 / 16 bf16 contributions) and
+# every remainder piece of 8, 4, 2 and 1 after them or alone
+@pytest.mark.parametrize("W", [5, 9, 10, 11, 13, 14, 15, 17, 23, 27, 31, 32, 33, 47, 63, 64])
 @pytest.mark.parametrize("gdtype,mode", [("f32", "fp32"), ("bf16", "fixed"),
                                          ("f32", "fixed"), ("bf16", "fp32")])
 def test_fused_runtime_worker_counts(W, gdtype, mode):
@@ -290,7 +292,8 @@ def test_adam_step_division_and_sqrt_across_magnitudes():
 # ----------------------------------------------------------- the three calls --
 @pytest.mark.parametrize("W,gdtype,mode", [(8, "f32", "fp32"), (16, "bf16", "fp32"),
                                            (8, "f32", "fixed"), (5, "bf16", "fixed"),
-                                           (1, "f32", "fp32")])
+                                           (1, "f32", "fp32"), (27, "bf16", "fp32"),
+                                           (31, "f32", "fixed"), (40, "bf16", "fixed")])
 def test_aggregate_matches_oracle(W, gdtype, mode):
     import paper_2409_00918_amd as dd
     t_ = torch()
