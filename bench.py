@@ -126,9 +126,19 @@ def copy_ceiling_gbps(elems=1 << 30, reps=10):
     compared with, next to the datasheet peak."""
     import numpy as np
     import torch
+    import paper_2409_00918_amd as dd
     L = probe_lib()
-    src = torch.ones(elems, device="cuda")
-    dst = torch.empty_like(src)
+    # in the same kind of memory as the shard: one physically contiguous
+    # block holding both buffers when the runtime has one
+    nbytes = elems * 4
+    gap = 64 << 20
+    slab = dd.contiguous_bytes(2 * nbytes + gap, "cuda")
+    if slab is not None:
+        src = slab[:nbytes].view(torch.float32).fill_(1.0)
+        dst = slab[nbytes + gap: 2 * nbytes + gap].view(torch.float32)
+    else:
+        src = torch.ones(elems, device="cuda")
+        dst = torch.empty_like(src)
     s = torch.cuda.current_stream()
     assert L.disdp_probe_copy(src.data_ptr(), dst.data_ptr(), elems * 4, s.cuda_stream or None) == 0
     torch.cuda.synchronize()
@@ -140,7 +150,7 @@ def copy_ceiling_gbps(elems=1 << 30, reps=10):
         b.record(s)
     torch.cuda.synchronize()
     ms = float(np.median([a.elapsed_time(b) for a, b in ev]))
-    del src, dst
+    del src, dst, slab
     torch.cuda.empty_cache()
     return round(2 * elems * 4 / (ms * 1e-3) / 1e9, 1)
 

@@ -15,7 +15,8 @@ call raises.
 ``aggregate_adam``  -- both in one pass               (disdp_aggregate_adam)
 ``quantize``        -- a worker's float -> int32 conversion (disdp_quantize)
 ``allocate_shard``  -- one device allocation holding a shard's arrays, placed
-                       by disdp_shard_layout
+                       by disdp_shard_layout (``contiguous_bytes``: such an
+                       allocation, physically contiguous)
 ``aggregate_adam_dev``, ``step_scalars``
                     -- the fused call with the step's constants read from
                        device memory (one HIP graph for every step)
@@ -462,9 +463,10 @@ class _ContiguousSlab:
         self.ptr = 0
 
 
-def _contiguous_bytes(nbytes: int, device):
-    """A uint8 device tensor over a physically contiguous allocation, or
-    None when the runtime has no such block (or torch cannot wrap it)."""
+def contiguous_bytes(nbytes: int, device="cuda"):
+    """A uint8 device tensor of `nbytes` over one physically contiguous
+    allocation (freed with its last view), or None when the runtime has no
+    such block (or torch cannot wrap it)."""
     torch = _torch()
     dev = torch.device(device)
     idx = dev.index if dev.index is not None else torch.cuda.current_device()
@@ -502,7 +504,7 @@ class Shard:
         torch = _torch()
         offs, total = shard_layout(n, W, gdtype, bf16_copy=bf16_copy, agg_f32=agg_f32,
                                    agg_i32=agg_i32)
-        slab = _contiguous_bytes(total, device) if contiguous and total > 0 else None
+        slab = contiguous_bytes(total, device) if contiguous and total > 0 else None
         self.contiguous = slab is not None
         self.slab = slab if slab is not None else \
             torch.empty(total, dtype=torch.uint8, device=device)
