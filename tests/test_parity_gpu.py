@@ -1026,3 +1026,32 @@ def test_contiguous_shard_slab_lifetime():
     t_.cuda.synchronize()
     free3, _ = t_.cuda.mem_get_info()
     assert free0 - free3 < total // 2             # returned
+
+
+def test_shard_falls_back_to_the_caching_allocator(monkeypatch):
+    """Without a physically contiguous block (refused by the runtime, here
+    forced) or with contiguous=False, the shard lives in torch's caching
+    allocator at the same planned offsets and computes the same bits."""
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    n, W = 70_001, 3
+    gs = synth.host_grads(640, 1, W, n, 1e-4)
+    p, m, v = synth.host_state(640, n, mv_sigma=1e-4)
+    want = oracle.fused(gs, p, m, v, t=2, **HP)
+    shards = [dd.allocate_shard(n, W, "f32", contiguous=False)]
+    monkeypatch.setattr(dd, "contiguous_bytes", lambda nbytes, device="cuda": None)
+    shards.append(dd.allocate_shard(n, W, "f32"))
+    offs, _ = dd.shard_layout(n, W, "f32")
+    for sh in shards:
+        assert not sh.contiguous
+        assert sh.param.data_ptr() == sh.slab.data_ptr() + offs[W]
+        for dst, src in zip(sh.grads, gs):
+            dst.copy_(to_dev(src))
+        for dst, src in ((sh.param, p), (sh.m, m), (sh.v, v)):
+            dst.copy_(to_dev(src))
+        dd.aggregate_adam(sh.grads, sh.param, sh.m, sh.v, sh.param_bf16, lr=HP["lr"],
+                          beta1=HP["beta1"], beta2=HP["beta2"], eps=HP["eps"],
+                          weight_decay=HP["wd"], step=2)
+        t_.cuda.synchronize()
+        assert_parity({"p": to_host(sh.param), "m": to_host(sh.m), "v": to_host(sh.v),
+                       "p16": to_host(sh.param_bf16)}, want, "caching-allocator shard")
