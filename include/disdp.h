@@ -41,7 +41,8 @@
  *             kernels over the host link -- e.g. the 12-byte states of a
  *             shard too large for HBM, kept in host DRAM as the paper's
  *             parameter server keeps them (Section III-D, steps 4 and 6).
- * Layout      Every array is flat and contiguous with N elements; index i
+ * Layout      Every array is flat and contiguous with N elements
+ *             (0 <= N <= 2^56, else DISDP_ERR_INVALID_ARG); index i
  *             is the same parameter in every array.  fp32 arrays hold IEEE
  *             binary32; bf16 arrays hold raw bf16 bit patterns (uint16_t);
  *             the int32 aggregate is two's complement.
@@ -50,7 +51,9 @@
  *             hipStreamSynchronize or an event.  A call enqueues kernel
  *             launches only (no allocation, memset, copy or wait), so it
  *             may be captured in a HIP graph; the hyperparameters, step t
- *             included, are kernel arguments and are fixed at capture.
+ *             included, are kernel arguments and are fixed at capture
+ *             (disdp_aggregate_adam_dev reads them from device memory when
+ *             its kernel runs instead).
  * Alignment   Any alignment is accepted; results never depend on it.  The
  *             vector kernels run when every array starts the same number of
  *             elements past a 4-element boundary (16 bytes for 4-byte
