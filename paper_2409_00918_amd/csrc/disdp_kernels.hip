@@ -485,7 +485,8 @@ __device__ __forceinline__ void process_element(const LaunchArgs &a, int64_t i)
 // W == 0: run-time worker count, one group per lane.  Groups [0, n/4) go
 // grid-stride in tiles of kBlock*U groups; the groups after the last full
 // tile go one per lane; the last n % 4 elements and the a.head elements
-// before the (vector-aligned) pointers go to lanes of block 0.
+// before the (advanced) pointers go to lanes of block 0.  Every pointer is
+// on a 4-byte boundary; the front end chose the head.
 template <int W, int GT, int MODE, bool ADAM, int U>
 __global__ DISDP_LAUNCH_BOUNDS void vector_kernel(LaunchArgs a)
 {
@@ -527,13 +528,14 @@ __global__ DISDP_LAUNCH_BOUNDS void vector_kernel(LaunchArgs a)
     }
     if (blockIdx.x == 0 && threadIdx.x < (a.n & 3))
         process_element<GT, MODE, ADAM>(a, (n_groups << 2) + threadIdx.x);
-    // the elements before the vector-aligned pointers
+    // the elements before the advanced pointers
     if (blockIdx.x == 0)
         for (int j = threadIdx.x; j < a.head; j += kBlock)
             process_element<GT, MODE, ADAM>(a, static_cast<int64_t>(j) - a.head);
 }
 
-// Element-wise kernel for buffers that are not vector aligned.
+// Element-wise kernel, for an array not aligned to its element size or bf16
+// arrays that no head puts on 4-byte boundaries together.
 template <int GT, int MODE, bool ADAM>
 __global__ DISDP_LAUNCH_BOUNDS void element_kernel(LaunchArgs a)
 {

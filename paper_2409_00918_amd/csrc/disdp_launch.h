@@ -31,7 +31,7 @@ struct LaunchArgs {
     int32_t *agg_i32;      // optional int32 aggregate (fixed mode)
     int64_t n;             // elements from the pointers on
     int head;              // 0-255 elements just before the pointers, done one
-                           // by one (pointers advanced to vector alignment)
+                           // by one (the pointers advanced past them)
     int W, gdtype, mode, frac_bits;
     float qscale, dqscale; // 2^k and 2^-k (fixed mode)
     StepScalars s;
@@ -40,7 +40,8 @@ struct LaunchArgs {
 };
 
 // Enqueues the kernel for `a` on `stream`.  `vector_path` selects the
-// 4-elements-per-lane kernels (all pointers suitably aligned).
+// 4-elements-per-lane kernels (every pointer, after the head, on a 4-byte
+// boundary).
 hipError_t launch(const LaunchArgs &a, Kind kind, bool vector_path,
                   hipStream_t stream);
 
