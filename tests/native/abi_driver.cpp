@@ -5,7 +5,11 @@
 //
 //   abi_driver <path to liboracle.so>
 //
-// Prints one line per case and "abi_driver: all ok" at the end; exits 1 on
+// Cases: the fused call over several steps (device and pinned host state),
+// one HIP graph replayed across optimizer steps, the conversion feeding
+// int32 contributions, a planned shard, virtual-memory-API memory, and the
+// error paths.  Prints one line per case and "abi_driver: all ok" at the
+// end; exits 1 on
 // the first mismatch, 2 on a HIP or setup error.  Inputs are a splitmix64
 // counter hash of (seed, index) mapped to [-1, 1) and scaled, with a sparse
 // x100 outlier tail: the same host bytes go to the oracle and to the GPU.
@@ -235,6 +239,93 @@ void fused_case(const char *label, int W, int gdtype, int64_t n, int mode, int k
         HIP_OK(hipFree(daf));
     if (dai)
         HIP_OK(hipFree(dai));
+    HIP_OK(hipStreamDestroy(s));
+}
+
+// One HIP graph for every optimizer step: a copy node refreshes the step's
+// constants (disdp_step_scalars, written into pinned host memory before each
+// replay) in device memory, then disdp_aggregate_adam_dev reads them.  Fresh
+// contributions are copied in eagerly between replays; every step is
+// compared with the oracle.
+void graph_case(const char *label, int W, int gdtype, int64_t n, int mode, int k, int steps)
+{
+    hipStream_t s;
+    HIP_OK(hipStreamCreate(&s));
+    std::vector<float> p(n), m(n), v(n);
+    for (int64_t i = 0; i < n; ++i) {
+        p[i] = draw(7101, i, 0.02f);
+        m[i] = draw(7102, i, 1e-4f);
+        const float r = draw(7103, i, 1e-4f);
+        v[i] = r * r;
+    }
+    const size_t gb = static_cast<size_t>(n) * (gdtype == DISDP_DT_BF16 ? 2 : 4);
+    const size_t fb = static_cast<size_t>(n) * 4;
+    std::vector<void *> dg(W);
+    for (int w = 0; w < W; ++w)
+        HIP_OK(hipMalloc(&dg[w], gb));
+    float *dp, *dm, *dv;
+    uint16_t *d16;
+    disdp_step_scalars_t *dsc, *hsc;
+    HIP_OK(hipMalloc(&dp, fb));
+    HIP_OK(hipMalloc(&dm, fb));
+    HIP_OK(hipMalloc(&dv, fb));
+    HIP_OK(hipMalloc(&d16, n * 2));
+    HIP_OK(hipMalloc(&dsc, sizeof *dsc));
+    HIP_OK(hipHostMalloc(reinterpret_cast<void **>(&hsc), sizeof *hsc, hipHostMallocDefault));
+    HIP_OK(hipMemcpy(dp, p.data(), fb, hipMemcpyDefault));
+    HIP_OK(hipMemcpy(dm, m.data(), fb, hipMemcpyDefault));
+    HIP_OK(hipMemcpy(dv, v.data(), fb, hipMemcpyDefault));
+
+    hipGraph_t graph;
+    hipGraphExec_t exec;
+    HIP_OK(hipStreamBeginCapture(s, hipStreamCaptureModeGlobal));
+    HIP_OK(hipMemcpyAsync(dsc, hsc, sizeof *dsc, hipMemcpyHostToDevice, s));
+    const disdp_status_t cst =
+        disdp_aggregate_adam_dev(dg.data(), W, static_cast<disdp_dtype_t>(gdtype), n,
+                                 static_cast<disdp_agg_mode_t>(mode), k, dp, dm, dv, d16,
+                                 nullptr, nullptr, dsc, s);
+    HIP_OK(hipStreamEndCapture(s, &graph));
+    expect(cst, DISDP_OK, label);
+    HIP_OK(hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0));
+
+    std::vector<uint16_t> want16(n), got16(n);
+    std::vector<float> gp(n), gm(n), gv(n);
+    Hp h;
+    bool ok = cst == DISDP_OK;
+    for (int t = 1; t <= steps && ok; ++t) {
+        HostGrads g(W, gdtype, n, 2000 + t, 1e-4f);
+        std::vector<const void *> hp_ptrs(W);
+        for (int w = 0; w < W; ++w) {
+            HIP_OK(hipMemcpy(dg[w], g.ptr(w), gb, hipMemcpyDefault));
+            hp_ptrs[w] = g.ptr(w);
+        }
+        const disdp_adamw_hparams_t hp = hparams(h, t);
+        expect(disdp_step_scalars(&hp, hsc), DISDP_OK, label);
+        HIP_OK(hipGraphLaunch(exec, s));
+        HIP_OK(hipStreamSynchronize(s));
+        oracle_fused(hp_ptrs.data(), W, gdtype, n, mode, k, p.data(), m.data(), v.data(),
+                     want16.data(), nullptr, nullptr, h.lr, h.b1, h.b2, h.eps, h.wd, t, 1.0f);
+        HIP_OK(hipMemcpy(gp.data(), dp, fb, hipMemcpyDefault));
+        HIP_OK(hipMemcpy(gm.data(), dm, fb, hipMemcpyDefault));
+        HIP_OK(hipMemcpy(gv.data(), dv, fb, hipMemcpyDefault));
+        HIP_OK(hipMemcpy(got16.data(), d16, n * 2, hipMemcpyDefault));
+        ok = same(gp.data(), p.data(), fb, "p", label) && ok;
+        ok = same(gm.data(), m.data(), fb, "m", label) && ok;
+        ok = same(gv.data(), v.data(), fb, "v", label) && ok;
+        ok = same(got16.data(), want16.data(), n * 2, "p16", label) && ok;
+    }
+    std::printf("%s %s: W=%d n=%lld replays=%d\n", ok ? "ok" : "FAIL", label, W,
+                static_cast<long long>(n), steps);
+    HIP_OK(hipGraphExecDestroy(exec));
+    HIP_OK(hipGraphDestroy(graph));
+    for (int w = 0; w < W; ++w)
+        HIP_OK(hipFree(dg[w]));
+    HIP_OK(hipFree(dp));
+    HIP_OK(hipFree(dm));
+    HIP_OK(hipFree(dv));
+    HIP_OK(hipFree(d16));
+    HIP_OK(hipFree(dsc));
+    HIP_OK(hipHostFree(hsc));
     HIP_OK(hipStreamDestroy(s));
 }
 
@@ -475,6 +566,10 @@ int main(int argc, char **argv)
     std::fflush(stdout);
     fused_case("fp32 W=3 pinned host state", 3, DISDP_DT_F32, 300007, DISDP_AGG_FP32, 0, 2, true,
                false);
+    std::fflush(stdout);
+    graph_case("graph replay fp32 W=6", 6, DISDP_DT_F32, 500009, DISDP_AGG_FP32, 0, 4);
+    std::fflush(stdout);
+    graph_case("graph replay fixed bf16 W=13", 13, DISDP_DT_BF16, 200003, DISDP_AGG_FIXED, 24, 3);
     std::fflush(stdout);
     quantize_case(6, 500009, 24);
     std::fflush(stdout);
