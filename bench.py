@@ -15,6 +15,7 @@ lr 1e-4, betas (0.9, 0.95), eps 1e-8, weight decay 0.1.
     python bench.py --copy-probe        # plain 4 GiB device copy (counter scale)
     python bench.py --entry aggregate   # another entry point on the same shard
     python bench.py --entry fused_graph # the fused call replayed as one HIP graph
+    python bench.py --entry layers      # the shard updated tensor by tensor
 
 Prints one JSON line.  ``roofline`` prices the kernel against HBM bandwidth
 (8 TB/s) with algorithmic bytes (each byte the call must move, counted once);
@@ -559,6 +560,97 @@ def run_entry(args):
                                    "algorithmic_bytes_per_element": bpe}}), flush=True)
 
 
+def run_layers(args):
+    """The 7B/8 shard updated tensor by tensor, as a parameter server walks
+    a model: one fused call per parameter tensor of OPT-6.7B (1/8 of each:
+    322 sub-ranges of the shard's flat arrays at their natural offsets, 512
+    to 25.7M elements, 832M in all), against one call over the same
+    elements.  Per step, timed with events on the launch stream and
+    interleaved over four rounds: (a) one call; (b) the 322 calls enqueued
+    eagerly from Python; (c) the 322 calls (disdp_aggregate_adam_dev)
+    captured once as a HIP graph, replayed per step after a copy node
+    refreshes the step's constants."""
+    import numpy as np
+    import torch
+    import paper_2409_00918_amd as dd
+    import synth
+    wl = synth.WORKLOADS[DEFAULT_WORKLOAD]
+    torch.cuda.set_device(0)
+    dd.lib()
+    sizes = synth.opt_tensor_shards()
+    total = sum(sizes)
+    if total > wl.n:
+        raise SystemExit("the tensor list does not fit the shard")
+    sh = allocate(wl)
+    hp = hparams(wl)
+    kw = dict(lr=hp["lr"], beta1=hp["beta1"], beta2=hp["beta2"], eps=hp["eps"],
+              weight_decay=hp["wd"])
+    offs = np.concatenate([[0], np.cumsum(sizes)[:-1]]).tolist()
+
+    def cut(o, k):
+        return ([g[o:o + k] for g in sh.grads], sh.param[o:o + k], sh.m[o:o + k],
+                sh.v[o:o + k], sh.param_bf16[o:o + k])
+
+    whole_args = cut(0, total)
+    tensor_args = [cut(o, k) for o, k in zip(offs, sizes)]
+    host = torch.zeros(10, dtype=torch.float32, pin_memory=True)
+    dev = torch.zeros(10, dtype=torch.float32, device="cuda")
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=side):
+        dev.copy_(host, non_blocking=True)
+        for g, p, m, v, p16 in tensor_args:
+            dd.aggregate_adam_dev(g, p, m, v, p16, scalars=dev)
+    torch.cuda.synchronize()
+    s = torch.cuda.current_stream()
+
+    def one(t):
+        g, p, m, v, p16 = whole_args
+        dd.aggregate_adam(g, p, m, v, p16, step=t, **kw)
+
+    def eager(t):
+        for g, p, m, v, p16 in tensor_args:
+            dd.aggregate_adam(g, p, m, v, p16, step=t, **kw)
+
+    def replay(t):
+        graph.replay()
+
+    def prepare(t, mode):
+        torch.cuda.synchronize()            # a previous replay has read `host`
+        if mode == "graph_per_tensor":
+            host.copy_(torch.frombuffer(bytearray(dd.step_scalars(step=t, **kw)),
+                                        dtype=torch.float32))
+
+    modes = {"one_call": one, "eager_per_tensor": eager, "graph_per_tensor": replay}
+    res = {k: [] for k in modes}
+    t = 0
+    for rnd in range(4 + 1):
+        for name, fn in modes.items():
+            for _ in range(args.steps if rnd else 1):
+                t += 1
+                prepare(t, name)
+                a = torch.cuda.Event(enable_timing=True)
+                b = torch.cuda.Event(enable_timing=True)
+                a.record(s)
+                fn(t)
+                b.record(s)
+                torch.cuda.synchronize()
+                if rnd:                      # round 0 warms every mode up
+                    res[name].append(a.elapsed_time(b))
+    out = {}
+    for name, v in res.items():
+        ms = float(np.median(v))
+        out[name] = {"ms_per_step": round(ms, 4), "G_params_s": round(total / ms / 1e6, 2),
+                     "TBps": round(total * 58 / ms / 1e9, 3)}
+    print(json.dumps({"metric": "G params/s, a 7B/8 shard updated tensor by tensor",
+                      "tensors": len(sizes), "elements": total,
+                      "smallest_tensor": min(sizes), "largest_tensor": max(sizes),
+                      "config": {"workload": wl.name, "W": wl.W, "grad_dtype": wl.gdtype,
+                                 "tensors": "OPT-6.7B parameter tensors, 1/8 of each"},
+                      "steps_per_mode": 4 * args.steps, **out}), flush=True)
+
+
 def _cu_mask_stream(first_cu: int, count: int, total: int):
     """A default-priority stream restricted to CUs [first_cu, first_cu+count)
     (hipExtStreamCreateWithCUMask on torch's HIP runtime), wrapped for torch."""
@@ -734,7 +826,7 @@ def main(argv=None):
     ap.add_argument("--contributions", choices=["float", "i32"], default="float",
                     help="i32: feed the fused call pre-quantised contributions")
     ap.add_argument("--entry", choices=["fused", "aggregate", "adam_step", "two_call",
-                                        "fused_graph"],
+                                        "fused_graph", "layers"],
                     default="fused",
                     help="time another entry point on the same shard (not the headline)")
     args = ap.parse_args(argv)
@@ -752,6 +844,8 @@ def main(argv=None):
         run_quantize(args)
     elif args.host_state:
         run_host_state(args)
+    elif args.entry == "layers":
+        run_layers(args)
     elif args.entry != "fused":
         run_entry(args)
     else:

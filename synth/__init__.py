@@ -67,6 +67,24 @@ WORKLOADS = {
 }
 
 
+def opt_tensor_shards(hidden: int = 4096, ffn: int = 16384, layers: int = 32,
+                      vocab: int = 50272, positions: int = 2048, shards: int = 8):
+    """Element counts of one data-parallel shard (1/shards, rounded up) of
+    each parameter tensor of an OPT-style decoder, in model order: token and
+    position embeddings, then per layer the fused QKV weight and bias, the
+    output projection and bias, the first LayerNorm (weight and bias), the
+    two MLP weights and biases, and the second LayerNorm.  The defaults are
+    OPT-6.7B's shapes (about 6.66e9 parameters, 8.3e8 per shard of 8)."""
+    def cut(x):
+        return -(-x // shards)
+    sizes = [cut(vocab * hidden), cut(positions * hidden)]
+    for _ in range(layers):
+        sizes += [cut(3 * hidden * hidden), cut(3 * hidden), cut(hidden * hidden), cut(hidden),
+                  cut(2 * hidden), cut(hidden * ffn), cut(ffn), cut(ffn * hidden), cut(hidden),
+                  cut(2 * hidden)]
+    return sizes
+
+
 def seed_for(wid: int, step: int, stream: int) -> int:
     """A 63-bit seed per (workload, step, stream); stream < 1000 are workers,
     1000 is the master weights, 1001+ are auxiliary draws."""
