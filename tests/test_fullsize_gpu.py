@@ -192,3 +192,55 @@ def test_grids_beyond_2_to_the_32_lanes():
     assert np.array_equal(got, want)
     del out, g
     t_.cuda.empty_cache()
+
+
+def test_full_size_graph_replayed_across_steps():
+    """The 7B/8 shard driven by one captured HIP graph (copy node for the
+    step's constants + disdp_aggregate_adam_dev), replayed for 5 steps with
+    fresh seeded contributions written between replays: sampled elements
+    against the oracle every step, and the bf16 copy checked everywhere."""
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    wl = synth.WORKLOADS["opt7b_shard8_w8_f32"]
+    free, _ = t_.cuda.mem_get_info()
+    if bytes_needed(wl) > 0.92 * free:
+        pytest.skip("not enough device memory")
+    n, W = wl.n, wl.W
+    sh = dd.allocate_shard(n, W, wl.gdtype)
+    dp, dm, dv = synth.device_state(wl.wid, n, wl.p_sigma, out=(sh.param, sh.m, sh.v))
+    idx = sample_indices(n, 91)
+    ix = t_.from_numpy(idx).cuda()
+    hp = dict(lr=np.float32(wl.lr), beta1=np.float32(wl.beta1), beta2=np.float32(wl.beta2),
+              eps=np.float32(wl.eps), wd=np.float32(wl.wd))
+    kw = dict(lr=hp["lr"], beta1=hp["beta1"], beta2=hp["beta2"], eps=hp["eps"],
+              weight_decay=hp["wd"])
+    host = t_.zeros(10, dtype=t_.float32, pin_memory=True)
+    dev = t_.zeros(10, dtype=t_.float32, device="cuda")
+    t_.cuda.synchronize()
+    side = t_.cuda.Stream()
+    graph = t_.cuda.CUDAGraph()
+    with t_.cuda.graph(graph, stream=side):
+        dev.copy_(host, non_blocking=True)
+        dd.aggregate_adam_dev(sh.grads, dp, dm, dv, sh.param_bf16, scalars=dev)
+    t_.cuda.synchronize()
+    p, m, v = (to_host(x[ix]) for x in (dp, dm, dv))
+    try:
+        for t in range(1, 6):
+            synth.device_grads(wl.wid, 200 + t, W, n, wl.sigma, outlier_frac=wl.outlier_frac,
+                               outlier_scale=wl.outlier_scale, out=sh.grads)
+            gs = [to_host(g[ix]) for g in sh.grads]
+            host.copy_(t_.frombuffer(bytearray(dd.step_scalars(step=t, **kw)),
+                                     dtype=t_.float32))
+            t_.cuda.synchronize()
+            graph.replay()
+            t_.cuda.synchronize()
+            want = oracle.fused(gs, p, m, v, t=t, **hp)
+            got = {"p": to_host(dp[ix]), "m": to_host(dm[ix]), "v": to_host(dv[ix]),
+                   "p16": to_host(sh.param_bf16[ix])}
+            assert_parity(got, want, f"graph replay step {t}")
+            assert t_.equal(dp.to(t_.bfloat16).view(t_.int16), sh.param_bf16), f"step {t}: p16"
+            p, m, v = want["p"], want["m"], want["v"]
+            print(f"[fullsize] graph replay step {t} ok", flush=True)
+    finally:
+        del graph, dp, dm, dv, sh
+        t_.cuda.empty_cache()
