@@ -569,7 +569,9 @@ def run_layers(args):
     interleaved over four rounds: (a) one call; (b) the 322 calls enqueued
     eagerly from Python; (c) the 322 calls (disdp_aggregate_adam_dev)
     captured once as a HIP graph, replayed per step after a copy node
-    refreshes the step's constants."""
+    refreshes the step's constants; (d) one disdp_aggregate_adam_multi call
+    (a batch of tensors per launch); (e) that call with the constants in
+    device memory, captured once as a HIP graph with its copy node."""
     import numpy as np
     import torch
     import paper_2409_00918_amd as dd
@@ -616,13 +618,37 @@ def run_layers(args):
     def replay(t):
         graph.replay()
 
+    # the multi-tensor call with its host arrays built once (the library
+    # still checks every pointer on every call)
+    mgrads = [g.data_ptr() for ta in tensor_args for g in ta[0]]
+    mns = [ta[1].numel() for ta in tensor_args]
+    mp, mm, mv, m16 = ([ta[i].data_ptr() for ta in tensor_args] for i in (1, 2, 3, 4))
+
+    mgraph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(mgraph, stream=side):
+        dev.copy_(host, non_blocking=True)
+        dd.aggregate_adam_multi(tensor_args, scalars=dev)
+    torch.cuda.synchronize()
+
+    def mreplay(t):
+        mgraph.replay()
+
+    def multi(t):
+        st = dd.raw_aggregate_adam_multi(
+            mgrads, wl.W, dd.DT_F32, len(tensor_args), mns, dd.AGG_FP32, 0, mp, mm, mv, m16,
+            dd.AdamWHParams(kw["lr"], kw["beta1"], kw["beta2"], kw["eps"], kw["weight_decay"],
+                            t, 1.0), s.cuda_stream)
+        if st != dd.OK:
+            raise dd.DisdpError(st, "disdp_aggregate_adam_multi")
+
     def prepare(t, mode):
         torch.cuda.synchronize()            # a previous replay has read `host`
-        if mode == "graph_per_tensor":
+        if mode in ("graph_per_tensor", "multi_tensor_graph"):
             host.copy_(torch.frombuffer(bytearray(dd.step_scalars(step=t, **kw)),
                                         dtype=torch.float32))
 
-    modes = {"one_call": one, "eager_per_tensor": eager, "graph_per_tensor": replay}
+    modes = {"one_call": one, "eager_per_tensor": eager, "graph_per_tensor": replay,
+             "multi_tensor_call": multi, "multi_tensor_graph": mreplay}
     res = {k: [] for k in modes}
     t = 0
     for rnd in range(4 + 1):

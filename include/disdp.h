@@ -22,7 +22,10 @@
  *   disdp_step_scalars, disdp_aggregate_adam_dev
  *                        -- the fused call with the step's constants in
  *                           device memory, for one HIP graph replayed
- *                           across optimizer steps.
+ *                           across optimizer steps;
+ *   disdp_aggregate_adam_multi
+ *                        -- the fused call over many tensors in separate
+ *                           buffers, a batch of tensors per launch.
  *
  * The calls follow the shape of the paper's asynchronous push/pull API
  * (Table II: a buffer pointer and a length; completion awaited through a
@@ -226,6 +229,42 @@ disdp_status_t disdp_aggregate_adam_dev(const void *const *grads, int W,
                                         float *agg_out_f32, int32_t *agg_out_i32,
                                         const disdp_step_scalars_t *scalars,
                                         hipStream_t stream);
+
+/* disdp_aggregate_adam over T tensors of one optimizer step (Section III-D,
+ * step 5, applied tensor by tensor): for a shard whose tensors live in
+ * separate buffers, one launch serves a batch of tensors instead of one
+ * launch each (up to 48 tensors and 320 pointers per launch).  Equal, bit
+ * for bit, to T disdp_aggregate_adam calls with the same hyperparameters.
+ *   T               number of tensors, 0 <= T <= 65536.
+ *   n               host array of T element counts (each 0 .. 2^56).
+ *   grads           host array of T*W device pointers: contribution w of
+ *                   tensor j is grads[j*W + w].
+ *   param, m, v     host arrays of T device pointers (fp32, updated in
+ *                   place).
+ *   param_bf16_out  host array of T device pointers (an entry may be NULL),
+ *                   or NULL: no bf16 copies.
+ *   hp              one step for every tensor, as in disdp_aggregate_adam;
+ *                   or NULL with `scalars` given.
+ *   scalars         NULL, or the step's constants in device memory as for
+ *                   disdp_aggregate_adam_dev (4-byte aligned, not
+ *                   overlapping an output), read when the kernels run: one
+ *                   captured HIP graph then serves every step.  Exactly one
+ *                   of hp and scalars is non-NULL.
+ * Every array is read before the call returns.  Tensors with n == 0 are
+ * skipped (their pointers may be NULL).  Checks as for disdp_aggregate_adam,
+ * over all tensors together: no output of any tensor may overlap any other
+ * buffer of any tensor (DISDP_ERR_ALIAS; contributions may overlap one
+ * another).  Alignment as for the other calls, per tensor.  The checks use
+ * host memory proportional to T * (W + 4); a launch failure after earlier
+ * batches were enqueued returns DISDP_ERR_HIP. */
+disdp_status_t disdp_aggregate_adam_multi(const void *const *grads, int W,
+                                          disdp_dtype_t gdtype, int T, const int64_t *n,
+                                          disdp_agg_mode_t mode, int frac_bits,
+                                          float *const *param, float *const *m,
+                                          float *const *v, uint16_t *const *param_bf16_out,
+                                          const disdp_adamw_hparams_t *hp,
+                                          const disdp_step_scalars_t *scalars,
+                                          hipStream_t stream);
 
 /* The float-to-integer format conversion a worker's NIC applies before
  * pushing its gradient to an integer-only switch (Section III-B "Format

@@ -20,6 +20,8 @@ call raises.
 ``aggregate_adam_dev``, ``step_scalars``
                     -- the fused call with the step's constants read from
                        device memory (one HIP graph for every step)
+``aggregate_adam_multi`` -- the fused call over many tensors in separate
+                       buffers (a batch of tensors per launch)
 """
 from __future__ import annotations
 
@@ -40,7 +42,8 @@ MAX_W = 64
 
 EXPORTS = ("disdp_aggregate", "disdp_adam_step", "disdp_aggregate_adam",
            "disdp_quantize", "disdp_shard_layout", "disdp_step_scalars",
-           "disdp_aggregate_adam_dev", "disdp_status_string")
+           "disdp_aggregate_adam_dev", "disdp_aggregate_adam_multi",
+           "disdp_status_string")
 LAYOUT_BF16_COPY, LAYOUT_AGG_F32, LAYOUT_AGG_I32 = 1, 2, 4
 
 
@@ -118,6 +121,9 @@ def lib() -> ctypes.CDLL:
         L.disdp_aggregate_adam_dev.restype = ci
         L.disdp_aggregate_adam_dev.argtypes = [vp, ci, ci, i64, ci, ci, vp, vp, vp, vp, vp, vp,
                                                vp, vp]
+        L.disdp_aggregate_adam_multi.restype = ci
+        L.disdp_aggregate_adam_multi.argtypes = [vp, ci, ci, ci, vp, ci, ci, vp, vp, vp, vp,
+                                                 ctypes.POINTER(AdamWHParams), vp, vp]
         L.disdp_status_string.restype = ctypes.c_char_p
         L.disdp_status_string.argtypes = [ci]
         _lib = L
@@ -172,6 +178,20 @@ def raw_aggregate_adam_dev(grad_ptrs, W, gdtype, n, mode, frac_bits, param, m, v
     return lib().disdp_aggregate_adam_dev(
         arr, W, gdtype, n, mode, frac_bits, param or None, m or None,
         v or None, p16 or None, agg_f32 or None, agg_i32 or None, scalars or None,
+        stream or None)
+
+
+def raw_aggregate_adam_multi(grad_ptrs, W, gdtype, T, ns, mode, frac_bits, params, ms, vs,
+                             p16s, hp: Optional[AdamWHParams], stream, scalars=0) -> int:
+    """Host arrays built from Python lists of integers (None = a NULL array)."""
+    def arr(xs, ctype=ctypes.c_void_p):
+        if xs is None:
+            return None
+        return (ctype * max(1, len(xs)))(*[(x or None) if ctype is ctypes.c_void_p else x
+                                           for x in xs])
+    return lib().disdp_aggregate_adam_multi(
+        arr(grad_ptrs), W, gdtype, T, arr(ns, ctypes.c_int64), mode, frac_bits, arr(params),
+        arr(ms), arr(vs), arr(p16s), None if hp is None else ctypes.byref(hp), scalars or None,
         stream or None)
 
 
@@ -371,6 +391,45 @@ def aggregate_adam_dev(grads, param, m, v, param_bf16_out=None, *, scalars,
         _dev_ptr(agg_out_i32, "agg_out_i32", n, (torch.int32,)),
         _dev_ptr(scalars, "scalars", ctypes.sizeof(StepScalars) // 4, f32))
     _check(st, "disdp_aggregate_adam_dev")
+
+
+def aggregate_adam_multi(tensors, *, lr=None, beta1=None, beta2=None, eps=None,
+                         weight_decay=None, step=None, grad_scale=1.0, scalars=None,
+                         mode="fp32", frac_bits: int = 0, stream=None) -> None:
+    """aggregate_adam over many tensors at once (a batch of tensors per
+    launch).  `tensors`: a sequence of (grads, param, m, v, param_bf16_out)
+    with grads a list of W contributions of that tensor's length and
+    param_bf16_out possibly None.  Every tensor takes the same step: the
+    hyperparameters, or `scalars` (as for aggregate_adam_dev) instead."""
+    torch = _torch()
+    tensors = list(tensors)
+    if not tensors:
+        return
+    W = len(tensors[0][0])
+    gdt = _grad_dtype(tensors[0][0][0])
+    allowed = {DT_F32: (torch.float32,), DT_I32: (torch.int32,)}.get(
+        gdt, (torch.bfloat16, torch.int16, torch.uint16))
+    f32 = (torch.float32,)
+    p16t = (torch.bfloat16, torch.int16, torch.uint16)
+    gp, ns, ps, ms_, vs, cs, every = [], [], [], [], [], [], []
+    for j, (grads, p, m, v, c) in enumerate(tensors):
+        if len(grads) != W:
+            raise ValueError(f"tensor {j} has {len(grads)} contributions, expected {W}")
+        n = p.numel()
+        gp += [_dev_ptr(g, f"tensors[{j}] grads[{w}]", n, allowed) for w, g in enumerate(grads)]
+        ns.append(n)
+        ps.append(_dev_ptr(p, f"tensors[{j}] param", n, f32))
+        ms_.append(_dev_ptr(m, f"tensors[{j}] m", n, f32))
+        vs.append(_dev_ptr(v, f"tensors[{j}] v", n, f32))
+        cs.append(_dev_ptr(c, f"tensors[{j}] param_bf16_out", n, p16t))
+        every += list(grads) + [p, m, v, c]
+    hp = None if scalars is not None else \
+        _hparams(lr, beta1, beta2, eps, weight_decay, step, grad_scale)
+    sc = _dev_ptr(scalars, "scalars", ctypes.sizeof(StepScalars) // 4, f32)
+    st = _launch(lambda *a: raw_aggregate_adam_multi(*a[:-1], stream=a[-1], scalars=sc),
+                 every + [scalars], stream, gp, W, gdt, len(tensors), ns,
+                 _mode(mode), frac_bits, ps, ms_, vs, cs if any(cs) else None, hp)
+    _check(st, "disdp_aggregate_adam_multi")
 
 
 def quantize(grad, out, *, frac_bits: int, stream=None) -> None:

@@ -4,10 +4,12 @@
 // include/disdp.h.
 #include "disdp.h"
 
+#include <algorithm>
 #include <cmath>
 #include <cstddef>
 #include <cstdint>
 #include <cstring>
+#include <vector>
 
 #include "disdp_launch.h"
 
@@ -327,6 +329,34 @@ disdp_status_t run(const void *const *grads, int W, int gdtype, int64_t n,
     return e == hipSuccess ? DISDP_OK : DISDP_ERR_HIP;
 }
 
+// Largest tensor count of disdp_aggregate_adam_multi.
+constexpr int kMaxTensors = 65536;
+
+// A byte interval [lo, hi) and whether the call writes it.
+struct Tagged {
+    uintptr_t lo, hi;
+    bool out;
+};
+
+// True when some written interval overlaps any other interval (written or
+// read); read intervals may overlap one another.  One sort and one sweep:
+// for a pair that overlaps, the later-starting interval starts before the
+// end of the earlier one, which the sweep keeps as the largest end so far.
+bool written_overlap(std::vector<Tagged> &spans)
+{
+    std::sort(spans.begin(), spans.end(),
+              [](const Tagged &a, const Tagged &b) { return a.lo < b.lo; });
+    uintptr_t max_end = 0, max_out_end = 0;
+    for (const Tagged &t : spans) {
+        if (t.lo < max_out_end || (t.out && t.lo < max_end))
+            return true;
+        max_end = std::max(max_end, t.hi);
+        if (t.out)
+            max_out_end = std::max(max_out_end, t.hi);
+    }
+    return false;
+}
+
 }  // namespace
 
 extern "C" {
@@ -390,6 +420,158 @@ disdp_status_t disdp_aggregate_adam_dev(const void *const *grads, int W,
                agg_out_f32, agg_out_i32, nullptr, /*adam=*/true,
                /*agg_f32_required=*/false, stream, /*scalars_in_memory=*/true,
                reinterpret_cast<const disdp::StepScalars *>(scalars));
+}
+
+disdp_status_t disdp_aggregate_adam_multi(const void *const *grads, int W,
+                                          disdp_dtype_t gdtype, int T, const int64_t *n,
+                                          disdp_agg_mode_t mode, int frac_bits,
+                                          float *const *param, float *const *m,
+                                          float *const *v, uint16_t *const *param_bf16_out,
+                                          const disdp_adamw_hparams_t *hp,
+                                          const disdp_step_scalars_t *scalars, hipStream_t stream)
+{
+    if (T < 0 || T > kMaxTensors)
+        return DISDP_ERR_INVALID_ARG;
+    disdp_status_t st = check_counts(W, gdtype, 0, mode, frac_bits);
+    if (st != DISDP_OK)
+        return st;
+    if ((hp != nullptr) == (scalars != nullptr))
+        return DISDP_ERR_INVALID_ARG;      // exactly one source of the constants
+    if (hp && (st = check_hparams(hp)) != DISDP_OK)
+        return st;
+    if (scalars && (reinterpret_cast<uintptr_t>(scalars) & 3))
+        return DISDP_ERR_INVALID_ARG;
+    if (T > 0 && !n)
+        return DISDP_ERR_INVALID_ARG;
+    bool any = false;
+    for (int j = 0; j < T; ++j) {
+        if (n[j] < 0 || n[j] > kMaxN)
+            return DISDP_ERR_INVALID_ARG;
+        any = any || n[j] > 0;
+    }
+    if (!any)
+        return DISDP_OK;
+
+    // NULL pointers, then overlap over every tensor's buffers at once
+    if (!grads || !param || !m || !v)
+        return DISDP_ERR_INVALID_ARG;
+    const int gb = grad_bytes(gdtype);
+    std::vector<Tagged> spans;
+    spans.reserve(static_cast<size_t>(T) * (W + 4));
+    for (int j = 0; j < T; ++j) {
+        if (n[j] == 0)
+            continue;
+        for (int w = 0; w < W; ++w) {
+            const void *g = grads[static_cast<int64_t>(j) * W + w];
+            if (!g)
+                return DISDP_ERR_INVALID_ARG;
+            const Span sp = span_of(g, n[j], gb);
+            spans.push_back({sp.lo, sp.hi, false});
+        }
+        if (!param[j] || !m[j] || !v[j])
+            return DISDP_ERR_INVALID_ARG;
+        const void *outs[] = {param[j], m[j], v[j]};
+        for (const void *o : outs) {
+            const Span sp = span_of(o, n[j], 4);
+            spans.push_back({sp.lo, sp.hi, true});
+        }
+        if (param_bf16_out && param_bf16_out[j]) {
+            const Span sp = span_of(param_bf16_out[j], n[j], 2);
+            spans.push_back({sp.lo, sp.hi, true});
+        }
+    }
+    if (scalars) {
+        const Span sp = span_of(scalars, 1, sizeof(disdp_step_scalars_t));
+        spans.push_back({sp.lo, sp.hi, false});
+    }
+    if (written_overlap(spans))
+        return DISDP_ERR_ALIAS;
+    if (scalars && !gpu_addressable(scalars))
+        return DISDP_ERR_INVALID_ARG;
+    for (int j = 0; j < T; ++j) {
+        if (n[j] == 0)
+            continue;
+        for (int w = 0; w < W; ++w)
+            if (!gpu_addressable(grads[static_cast<int64_t>(j) * W + w]))
+                return DISDP_ERR_INVALID_ARG;
+        if (!gpu_addressable(param[j]) || !gpu_addressable(m[j]) || !gpu_addressable(v[j]) ||
+            (param_bf16_out && param_bf16_out[j] && !gpu_addressable(param_bf16_out[j])))
+            return DISDP_ERR_INVALID_ARG;
+    }
+
+    // Batches of tensors per launch; a tensor the vector kernels cannot
+    // take goes through the single-tensor path (the element kernel).
+    disdp::MultiArgs ma;
+    std::memset(&ma, 0, sizeof ma);
+    ma.W = W;
+    ma.gdtype = gdtype;
+    ma.mode = mode;
+    ma.frac_bits = (mode == DISDP_AGG_FIXED) ? frac_bits : 0;
+    ma.qscale = std::ldexp(1.0f, ma.frac_bits);
+    ma.dqscale = std::ldexp(1.0f, -ma.frac_bits);
+    const disdp::StepScalars *s_dev = reinterpret_cast<const disdp::StepScalars *>(scalars);
+    if (hp)
+        ma.s = step_scalars(hp);
+    ma.s_dev = s_dev;
+    const int per_tensor = W + 4;
+    const int cap = std::min(disdp::kMultiMaxTensors, disdp::kMultiMaxPtrs / per_tensor);
+    auto flush = [&]() -> bool {
+        if (ma.count == 0)
+            return true;
+        const hipError_t e = disdp::launch_multi(ma, stream);
+        ma.count = 0;
+        return e == hipSuccess;
+    };
+    for (int j = 0; j < T; ++j) {
+        if (n[j] == 0)
+            continue;
+        const void *const *gj = grads + static_cast<int64_t>(j) * W;
+        uint16_t *p16 = param_bf16_out ? param_bf16_out[j] : nullptr;
+        const void *ptrs[disdp::kMaxW + 4];
+        int sizes[disdp::kMaxW + 4];
+        int np = 0;
+        for (int w = 0; w < W; ++w) {
+            ptrs[np] = gj[w];
+            sizes[np++] = gb;
+        }
+        const void *state[] = {param[j], m[j], v[j]};
+        for (const void *sp : state) {
+            ptrs[np] = sp;
+            sizes[np++] = 4;
+        }
+        if (p16) {
+            ptrs[np] = p16;
+            sizes[np++] = 2;
+        }
+        const int head = vector_head(ptrs, sizes, np, /*ref=*/W, n[j]);
+        if (head < 0) {
+            st = run(gj, W, gdtype, n[j], mode, frac_bits, param[j], m[j], v[j], p16, nullptr,
+                     nullptr, hp, /*adam=*/true, /*agg_f32_required=*/false, stream,
+                     /*scalars_in_memory=*/s_dev != nullptr, s_dev);
+            if (st != DISDP_OK)
+                return st;
+            continue;
+        }
+        if (ma.count == cap && !flush())
+            return DISDP_ERR_HIP;
+        const int c = ma.count;
+        void **slot = ma.ptr + c * per_tensor;
+        for (int w = 0; w < W; ++w)
+            slot[w] = const_cast<char *>(static_cast<const char *>(gj[w])) +
+                      static_cast<int64_t>(head) * gb;
+        slot[W] = param[j] + head;
+        slot[W + 1] = m[j] + head;
+        slot[W + 2] = v[j] + head;
+        slot[W + 3] = p16 ? p16 + head : nullptr;
+        ma.n[c] = n[j] - head;
+        ma.head[c] = head;
+        const int64_t groups = ma.n[c] >> 2;
+        const int64_t tiles =
+            std::max<int64_t>(1, (groups + disdp::kMultiTileGroups - 1) / disdp::kMultiTileGroups);
+        ma.tile_start[c + 1] = ma.tile_start[c] + tiles;
+        ma.count = c + 1;
+    }
+    return flush() ? DISDP_OK : DISDP_ERR_HIP;
 }
 
 disdp_status_t disdp_quantize(const void *grad, disdp_dtype_t gdtype, int64_t n,

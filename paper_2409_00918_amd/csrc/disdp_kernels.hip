@@ -191,7 +191,8 @@ __device__ __forceinline__ int32_t saturate32(int64_t s)
 
 // The step constants of a launch: by value in the arguments, or read from
 // memory when the kernel runs (one uniform load per wave, scalar cache).
-__device__ __forceinline__ StepScalars step_scalars_of(const LaunchArgs &a)
+template <class A>
+__device__ __forceinline__ StepScalars step_scalars_of(const A &a)
 {
     return a.s_dev ? *a.s_dev : a.s;
 }
@@ -310,8 +311,8 @@ struct Acc {
 
 // ---- writing one group's results -----------------------------------------
 
-template <int MODE, bool ADAM>
-__device__ __forceinline__ void finish_group(const LaunchArgs &a, int64_t grp, const float (&agg)[4],
+template <int MODE, bool ADAM, class A>
+__device__ __forceinline__ void finish_group(const A &a, int64_t grp, const float (&agg)[4],
                                              const int32_t (&ai)[4], f32x4 P, f32x4 M, f32x4 V)
 {
     if (a.agg_f32)
@@ -342,8 +343,8 @@ __device__ __forceinline__ void finish_group(const LaunchArgs &a, int64_t grp, c
 
 // Groups g0, g0 + stride, ..., g0 + (U-1) stride: every load first, then
 // the arithmetic, then the stores.
-template <int W, int GT, int MODE, bool ADAM, int U>
-__device__ __forceinline__ void process_groups(const LaunchArgs &a, int64_t g0, int stride)
+template <int W, int GT, int MODE, bool ADAM, int U, class A>
+__device__ __forceinline__ void process_groups(const A &a, int64_t g0, int stride)
 {
     typename Contrib<GT>::type c[U][W][4];
     f32x4 P[U], M[U], V[U];
@@ -381,8 +382,8 @@ __device__ __forceinline__ void process_groups(const LaunchArgs &a, int64_t g0, 
 // then the additions in worker order.  No branch separates the loads, so
 // none waits for the one before (a conditional load per contribution made
 // the compiler wait after each).  `first`: w0 is contribution 0.
-template <int K, int GT, int MODE>
-__device__ __forceinline__ void accumulate_piece(const LaunchArgs &a, int64_t grp, int w0,
+template <int K, int GT, int MODE, class A>
+__device__ __forceinline__ void accumulate_piece(const A &a, int64_t grp, int w0,
                                                  bool first, Acc<MODE> (&acc)[4])
 {
     typename Contrib<GT>::type c[K][4];
@@ -403,8 +404,8 @@ __device__ __forceinline__ void accumulate_piece(const LaunchArgs &a, int64_t gr
 
 // Contributions in chunks of 128 bytes per lane (8 fp32 or int32, 16 bf16),
 // then the remaining W mod chunk in pieces of 8, 4, 2 and 1.
-template <int GT, int MODE, bool ADAM>
-__device__ __forceinline__ void process_group_rt(const LaunchArgs &a, int64_t grp)
+template <int GT, int MODE, bool ADAM, class A>
+__device__ __forceinline__ void process_group_rt(const A &a, int64_t grp)
 {
     constexpr int kChunk = GT == kGradBF16 ? 16 : 8;
     f32x4 P{}, M{}, V{};
@@ -444,8 +445,8 @@ __device__ __forceinline__ void process_group_rt(const LaunchArgs &a, int64_t gr
 
 // ---- one element -----------------------------------------------------------
 
-template <int GT, int MODE, bool ADAM>
-__device__ __forceinline__ void process_element(const LaunchArgs &a, int64_t i)
+template <int GT, int MODE, bool ADAM, class A>
+__device__ __forceinline__ void process_element(const A &a, int64_t i)
 {
     Acc<MODE> acc;
     acc.first(load_one<GT>(a.g[0], i), a.qscale);
@@ -542,6 +543,76 @@ __global__ DISDP_LAUNCH_BOUNDS void element_kernel(LaunchArgs a)
     const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
     for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < a.n; i += stride)
         process_element<GT, MODE, ADAM>(a, i);
+}
+
+// ---- several tensors in one launch ------------------------------------------
+
+// Tensor j of a multi-tensor launch, with the members the group helpers
+// read from LaunchArgs (the contribution pointers stay in the argument
+// segment).
+struct TensorView {
+    const void *const *g;
+    float *p, *m, *v;
+    uint16_t *p16;
+    float *agg_f32;
+    int32_t *agg_i32;
+    float qscale, dqscale;
+    StepScalars s;
+    const StepScalars *s_dev;
+    int W;
+};
+
+// Fused aggregation + AdamW over the tensors of `ma`, one 256-element tile
+// per virtual block, grid-stride over the virtual blocks.  Per tensor as in
+// vector_kernel: whole groups one per lane, the last n % 4 elements by the
+// tensor's last tile, its head elements by its first tile.
+template <int W, int GT, int MODE>
+__global__ DISDP_LAUNCH_BOUNDS void multi_kernel(MultiArgs ma)
+{
+    const int64_t total = ma.tile_start[ma.count];
+    const int per_tensor = ma.W + 4;
+    for (int64_t vb = blockIdx.x; vb < total; vb += gridDim.x) {
+        int lo = 0, hi = ma.count - 1;   // the last j with tile_start[j] <= vb
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (ma.tile_start[mid] <= vb)
+                lo = mid;
+            else
+                hi = mid - 1;
+        }
+        const int j = lo;
+        void *const *tp = ma.ptr + j * per_tensor;
+        TensorView t;
+        t.g = const_cast<const void *const *>(tp);
+        t.p = static_cast<float *>(tp[ma.W]);
+        t.m = static_cast<float *>(tp[ma.W + 1]);
+        t.v = static_cast<float *>(tp[ma.W + 2]);
+        t.p16 = static_cast<uint16_t *>(tp[ma.W + 3]);
+        t.agg_f32 = nullptr;
+        t.agg_i32 = nullptr;
+        t.qscale = ma.qscale;
+        t.dqscale = ma.dqscale;
+        t.s = ma.s;
+        t.s_dev = ma.s_dev;
+        t.W = ma.W;
+        const int64_t n = ma.n[j];
+        const int64_t n_groups = n >> 2;
+        const int64_t tile = vb - ma.tile_start[j];
+        for (int l = threadIdx.x; l < kMultiTileGroups; l += kBlock) {
+            const int64_t grp = tile * kMultiTileGroups + l;
+            if (grp < n_groups) {
+                if constexpr (W > 0)
+                    process_groups<W, GT, MODE, true, 1>(t, grp, kBlock);
+                else
+                    process_group_rt<GT, MODE, true>(t, grp);
+            }
+        }
+        if (vb == ma.tile_start[j + 1] - 1 && threadIdx.x < (n & 3))
+            process_element<GT, MODE, true>(t, (n_groups << 2) + threadIdx.x);
+        if (tile == 0)
+            for (int e = threadIdx.x; e < ma.head[j]; e += kBlock)
+                process_element<GT, MODE, true>(t, static_cast<int64_t>(e) - ma.head[j]);
+    }
 }
 
 // ---- the format conversion as a producer ------------------------------------
@@ -859,6 +930,56 @@ hipError_t launch(const LaunchArgs &a, Kind kind, bool vector_path, hipStream_t 
 {
     return kind == kAggregateAdam ? dispatch<true>(a, vector_path, stream)
                                   : dispatch<false>(a, vector_path, stream);
+}
+
+namespace {
+
+template <int W, int GT, int MODE>
+hipError_t launch_multi_w(const MultiArgs &a, hipStream_t stream)
+{
+    constexpr int kGradBytes = GT == kGradBF16 ? 2 : 4;
+    constexpr int kLaneBytes = W > 0 ? 4 * (W * kGradBytes + 12) : 1 << 30;
+    constexpr bool kConverts = MODE == kAggFixed && GT != kGradI32;
+    const int base = W == 0    ? runtime_w_waves(a.W, GT, MODE)
+                     : kConverts ? fixed_mode_waves(kLaneBytes, GT == kGradBF16)
+                                 : fp32_mode_waves(kLaneBytes);
+    const int lds = occupancy_lds_bytes(blocks_per_cu_cap(base, stream));
+    const int64_t blocks = clamp_grid(a.tile_start[a.count], kBlock);
+    void *args[] = {const_cast<MultiArgs *>(&a)};
+    return hipLaunchKernel(reinterpret_cast<const void *>(&multi_kernel<W, GT, MODE>),
+                           dim3(static_cast<unsigned>(blocks)), dim3(kBlock), args,
+                           static_cast<size_t>(lds), stream);
+}
+
+template <int GT, int MODE>
+hipError_t launch_multi_gm(const MultiArgs &a, hipStream_t stream)
+{
+    switch (a.W) {
+    case 1: return launch_multi_w<1, GT, MODE>(a, stream);
+    case 2: return launch_multi_w<2, GT, MODE>(a, stream);
+    case 3: return launch_multi_w<3, GT, MODE>(a, stream);
+    case 4: return launch_multi_w<4, GT, MODE>(a, stream);
+    case 5: return launch_multi_w<5, GT, MODE>(a, stream);
+    case 6: return launch_multi_w<6, GT, MODE>(a, stream);
+    case 7: return launch_multi_w<7, GT, MODE>(a, stream);
+    case 8: return launch_multi_w<8, GT, MODE>(a, stream);
+    case 12: return launch_multi_w<12, GT, MODE>(a, stream);
+    case 16: return launch_multi_w<16, GT, MODE>(a, stream);
+    default: return launch_multi_w<0, GT, MODE>(a, stream);
+    }
+}
+
+}  // namespace
+
+hipError_t launch_multi(const MultiArgs &a, hipStream_t stream)
+{
+    if (a.gdtype == kGradI32)  // the front end admits int32 only in fixed mode
+        return launch_multi_gm<kGradI32, kAggFixed>(a, stream);
+    if (a.gdtype == kGradF32)
+        return a.mode == kAggFP32 ? launch_multi_gm<kGradF32, kAggFP32>(a, stream)
+                                  : launch_multi_gm<kGradF32, kAggFixed>(a, stream);
+    return a.mode == kAggFP32 ? launch_multi_gm<kGradBF16, kAggFP32>(a, stream)
+                              : launch_multi_gm<kGradBF16, kAggFixed>(a, stream);
 }
 
 hipError_t launch_quantize(const QuantizeArgs &q, bool vector_path, hipStream_t stream)

@@ -45,6 +45,29 @@ struct LaunchArgs {
 hipError_t launch(const LaunchArgs &a, Kind kind, bool vector_path,
                   hipStream_t stream);
 
+// Several tensors of one optimizer step in one launch: virtual block b of
+// the launch belongs to the last tensor j with tile_start[j] <= b, and is
+// tile b - tile_start[j] of it (256 elements).  The struct travels in the
+// kernel-argument segment and stays under 4 KiB.
+constexpr int kMultiMaxTensors = 48;
+constexpr int kMultiMaxPtrs = 320;
+constexpr int kMultiTileGroups = 64;  // 4-element groups per virtual block
+struct MultiArgs {
+    int count;                                  // tensors in this launch (>= 1)
+    int W, gdtype, mode, frac_bits;
+    float qscale, dqscale;                      // 2^k and 2^-k (fixed mode)
+    StepScalars s;
+    const StepScalars *s_dev;                   // as in LaunchArgs
+    int64_t tile_start[kMultiMaxTensors + 1];   // [count] = blocks in all
+    int64_t n[kMultiMaxTensors];                // elements from the pointers on
+    int head[kMultiMaxTensors];                 // 0-255 elements before them
+    void *ptr[kMultiMaxPtrs];                   // tensor j at j * (W + 4): the W
+                                                // contributions, p, m, v, bf16
+                                                // copy (may be NULL)
+};
+static_assert(sizeof(MultiArgs) <= 4096, "kernel arguments above 4 KiB");
+hipError_t launch_multi(const MultiArgs &a, hipStream_t stream);
+
 // The float-to-int32 format conversion of one buffer.
 struct QuantizeArgs {
     const void *g;     // n elements of gdtype (kGradF32 or kGradBF16)

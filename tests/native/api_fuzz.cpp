@@ -9,6 +9,9 @@
 //   * each entry point with exactly one argument error injected into an
 //     otherwise valid call: the documented status, and no launch (valid
 //     fused calls: the step constants passed by value, or by address only);
+//   * disdp_aggregate_adam_multi over random tensor lists: batch packing,
+//     per-tensor heads and pointers, the single-tensor fallback, injected
+//     errors;
 //   * valid calls whose arrays share, or do not share, a misalignment: the
 //     vector/element choice, the head of elements done one by one and the
 //     advanced pointers (on a common boundary, or every array on a 4-byte
@@ -21,6 +24,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <vector>
 
 #include "disdp.h"
 #include "disdp_launch.h"
@@ -33,6 +37,9 @@ bool g_addressable = true;
 disdp::LaunchArgs g_args;
 bool g_vec = false;
 disdp::QuantizeArgs g_qargs;
+std::vector<disdp::LaunchArgs> g_singles;  // every single-tensor launch
+std::vector<bool> g_single_vec;
+std::vector<disdp::MultiArgs> g_multis;    // every multi-tensor launch
 }  // namespace
 
 namespace disdp {
@@ -41,6 +48,14 @@ hipError_t launch(const LaunchArgs &a, Kind, bool vector_path, hipStream_t)
     ++g_launches;
     g_args = a;
     g_vec = vector_path;
+    g_singles.push_back(a);
+    g_single_vec.push_back(vector_path);
+    return hipSuccess;
+}
+hipError_t launch_multi(const MultiArgs &a, hipStream_t)
+{
+    ++g_launches;
+    g_multis.push_back(a);
     return hipSuccess;
 }
 hipError_t launch_quantize(const QuantizeArgs &q, bool vector_path, hipStream_t)
@@ -488,6 +503,188 @@ void fuzz_alignment(int iters)
     }
 }
 
+// ---- many tensors in one call ------------------------------------------------
+// Random tensor lists (sizes, worker counts, per-tensor phases, some tensors
+// empty, some with an element-misaligned array): every non-empty tensor must
+// be launched exactly once, either in one batch slot -- with its head, its
+// pointers advanced by the head onto 4-byte boundaries, its tile range
+// ceil((n - head) / 4 / 64) (at least 1) -- or, when no head fits, on its own
+// through the element kernel; batches within their capacity.  Then one
+// error per call: an output overlapping a buffer of another tensor, a NULL
+// pointer, a bad count.
+char *addr(int64_t slot) { return reinterpret_cast<char *>((uintptr_t(1) << 46) + (uintptr_t(slot) << 34)); }
+
+void fuzz_multi(int iters)
+{
+    for (int it = 0; it < iters; ++it) {
+        const int W = below(4) ? 1 + static_cast<int>(below(16)) : 1 + static_cast<int>(below(64));
+        const int mode = static_cast<int>(below(2));
+        const int gdt = mode == DISDP_AGG_FIXED ? static_cast<int>(below(3)) : static_cast<int>(below(2));
+        const int gb = gdt == DISDP_DT_BF16 ? 2 : 4;
+        const int T = static_cast<int>(below(120));
+        std::vector<int64_t> n(T);
+        std::vector<const void *> g(static_cast<size_t>(T) * W);
+        std::vector<float *> p(T), m(T), v(T);
+        std::vector<uint16_t *> p16(T);
+        std::vector<bool> odd(T, false);
+        const bool copies = below(4) != 0;
+        int64_t slot = 0;
+        for (int j = 0; j < T; ++j) {
+            n[j] = below(5) == 0 ? 0 : below(3) == 0 ? below(300) : below(1 << 20);
+            const int64_t phase = below(3) ? below(512) : 0;
+            const bool unrelated = below(4) == 0;
+            odd[j] = below(16) == 0;
+            for (int w = 0; w < W; ++w)
+                g[static_cast<size_t>(j) * W + w] =
+                    addr(slot++) + gb * (unrelated ? below(512) : phase) + (odd[j] && w == 0 ? 1 : 0);
+            p[j] = reinterpret_cast<float *>(addr(slot++) + 4 * phase);
+            m[j] = reinterpret_cast<float *>(addr(slot++) + 4 * (unrelated ? below(512) : phase));
+            v[j] = reinterpret_cast<float *>(addr(slot++) + 4 * phase);
+            p16[j] = copies && below(8) ? reinterpret_cast<uint16_t *>(addr(slot++) + 2 * phase)
+                                        : nullptr;
+        }
+        const disdp_adamw_hparams_t hp = {1e-4f, 0.9f, 0.95f, 1e-8f, 0.1f, 1 + below(1000), 1.0f};
+        // the step's constants by value, or in (fake) device memory
+        const bool dev = below(2) != 0;
+        const disdp_step_scalars_t *sc =
+            dev ? reinterpret_cast<const disdp_step_scalars_t *>(addr(slot++) + 4 * below(64))
+                : nullptr;
+        g_singles.clear();
+        g_single_vec.clear();
+        g_multis.clear();
+        const disdp_status_t st = disdp_aggregate_adam_multi(
+            g.data(), W, static_cast<disdp_dtype_t>(gdt), T, n.data(),
+            static_cast<disdp_agg_mode_t>(mode), 24, p.data(), m.data(), v.data(),
+            copies ? p16.data() : nullptr, dev ? nullptr : &hp, sc, nullptr);
+        CHECK(st == DISDP_OK, "multi: status %d (T=%d W=%d)", st, T, W);
+        if (st != DISDP_OK)
+            continue;
+        const int per = W + 4;
+        const int cap = std::min(disdp::kMultiMaxTensors, disdp::kMultiMaxPtrs / per);
+        std::vector<int> seen(T, 0);
+        for (const disdp::MultiArgs &ma : g_multis) {
+            CHECK(ma.count >= 1 && ma.count <= cap, "batch of %d tensors (cap %d)", ma.count, cap);
+            CHECK(ma.W == W && ma.tile_start[0] == 0, "batch header");
+            CHECK(dev ? (ma.s_dev == reinterpret_cast<const disdp::StepScalars *>(sc) && ma.s.b1 == 0.0f)
+                      : (!ma.s_dev && ma.s.b1 == hp.beta1),
+                  "batch step constants");
+            for (int c = 0; c < ma.count; ++c) {
+                const char *pp = static_cast<const char *>(ma.ptr[c * per + W]);
+                const int h = ma.head[c];
+                int j = -1;
+                for (int k = 0; k < T; ++k)
+                    if (n[k] > 0 && reinterpret_cast<const char *>(p[k]) + int64_t(h) * 4 == pp)
+                        j = k;
+                CHECK(j >= 0, "batch slot %d matches no tensor", c);
+                if (j < 0)
+                    continue;
+                ++seen[j];
+                CHECK(h >= 0 && h <= 255 && h <= n[j] && ma.n[c] + h == n[j],
+                      "tensor %d: head %d n %lld of %lld", j, h, (long long)ma.n[c], (long long)n[j]);
+                const int64_t tiles = std::max<int64_t>(1, ((ma.n[c] >> 2) + 63) / 64);
+                CHECK(ma.tile_start[c + 1] - ma.tile_start[c] == tiles, "tensor %d: tiles", j);
+                for (int w = 0; w < W; ++w) {
+                    const char *q = static_cast<const char *>(ma.ptr[c * per + w]);
+                    CHECK(q == static_cast<const char *>(g[static_cast<size_t>(j) * W + w]) + int64_t(h) * gb,
+                          "tensor %d contribution %d not advanced by the head", j, w);
+                    CHECK(ma.n[c] == 0 || reinterpret_cast<uintptr_t>(q) % 4 == 0,
+                          "tensor %d contribution %d off a 4-byte boundary", j, w);
+                }
+                CHECK(ma.ptr[c * per + W + 1] == m[j] + h && ma.ptr[c * per + W + 2] == v[j] + h,
+                      "tensor %d state not advanced", j);
+                CHECK((p16[j] && copies) ? ma.ptr[c * per + W + 3] == p16[j] + h
+                                         : ma.ptr[c * per + W + 3] == nullptr,
+                      "tensor %d copy pointer", j);
+            }
+        }
+        for (size_t i = 0; i < g_singles.size(); ++i) {
+            const disdp::LaunchArgs &a = g_singles[i];
+            int j = -1;
+            for (int k = 0; k < T; ++k)
+                if (n[k] > 0 && a.p == p[k] && a.n == n[k])
+                    j = k;
+            CHECK(j >= 0 && !g_single_vec[i], "single launch matches no tensor or is not elementwise");
+            CHECK(a.s_dev == reinterpret_cast<const disdp::StepScalars *>(sc),
+                  "single launch step constants");
+            if (j >= 0)
+                ++seen[j];
+        }
+        for (int j = 0; j < T; ++j)
+            CHECK(seen[j] == (n[j] > 0 ? 1 : 0), "tensor %d launched %d times (n %lld)", j, seen[j],
+                  (long long)n[j]);
+
+        // one injected error
+        int j0 = -1;
+        for (int k = 0; k < T; ++k)
+            if (n[k] > 8)
+                j0 = k;
+        if (j0 < 0)
+            continue;
+        const int kind = static_cast<int>(below(6));
+        disdp_status_t want = DISDP_OK;
+        std::vector<float *> p2 = p, m2 = m;
+        std::vector<const void *> g2 = g;
+        std::vector<int64_t> n2 = n;
+        int T2 = T;
+        if (kind == 0) {       // tensor j0's m inside another tensor's contribution
+            int k1 = -1;
+            for (int k = 0; k < T; ++k)
+                if (k != j0 && n[k] > 0)
+                    k1 = k;
+            if (k1 < 0)
+                continue;
+            m2[j0] = reinterpret_cast<float *>(const_cast<char *>(
+                static_cast<const char *>(g[static_cast<size_t>(k1) * W]) + gb * below(n[k1])));
+            want = DISDP_ERR_ALIAS;
+        } else if (kind == 1) {  // two tensors sharing a weight array
+            int k1 = -1;
+            for (int k = 0; k < T; ++k)
+                if (k != j0 && n[k] > 0)
+                    k1 = k;
+            if (k1 < 0)
+                continue;
+            p2[j0] = p[k1];
+            want = DISDP_ERR_ALIAS;
+        } else if (kind == 2) {  // a NULL contribution
+            g2[static_cast<size_t>(j0) * W + below(W)] = nullptr;
+            want = DISDP_ERR_INVALID_ARG;
+        } else if (kind == 3) {  // a negative count, or too many tensors
+            if (below(2))
+                n2[j0] = -1 - below(5);
+            else
+                T2 = 65537;
+            want = DISDP_ERR_INVALID_ARG;
+        } else if (kind == 4) {  // step constants: both sources, none, or misaligned
+            want = DISDP_ERR_INVALID_ARG;
+        } else {                 // device step constants inside an output
+            want = DISDP_ERR_ALIAS;
+        }
+        const disdp_adamw_hparams_t *hp2 = dev ? nullptr : &hp;
+        const disdp_step_scalars_t *sc2 = sc;
+        if (kind == 4) {
+            const int how = static_cast<int>(below(3));
+            const disdp_step_scalars_t *some =
+                reinterpret_cast<const disdp_step_scalars_t *>(addr(slot++));
+            hp2 = how == 0 ? &hp : nullptr;
+            sc2 = how == 0 ? some
+                  : how == 1 ? nullptr
+                             : reinterpret_cast<const disdp_step_scalars_t *>(
+                                   reinterpret_cast<const char *>(some) + 1 + below(3));
+        } else if (kind == 5) {
+            hp2 = nullptr;
+            sc2 = reinterpret_cast<const disdp_step_scalars_t *>(
+                reinterpret_cast<const char *>(v[j0]) + 4 * below(n[j0]));
+        }
+        const int before = g_launches;
+        const disdp_status_t st2 = disdp_aggregate_adam_multi(
+            g2.data(), W, static_cast<disdp_dtype_t>(gdt), T2, n2.data(),
+            static_cast<disdp_agg_mode_t>(mode), 24, p2.data(), m2.data(), v.data(),
+            copies ? p16.data() : nullptr, hp2, sc2, nullptr);
+        CHECK(st2 == want, "multi error kind %d: status %d want %d", kind, st2, want);
+        CHECK(g_launches == before, "multi error kind %d launched", kind);
+    }
+}
+
 }  // namespace
 
 int main()
@@ -495,6 +692,7 @@ int main()
     fuzz_layout(200000);
     fuzz_errors(200000);
     fuzz_alignment(100000);
+    fuzz_multi(3000);
     if (failures) {
         std::printf("api_fuzz: %d failures\n", failures);
         return 1;

@@ -425,3 +425,75 @@ def test_fused_dev_aliasing():
     # scalars overlapping a contribution are legal (both are read only); the
     # call then fails later on the fake, unmapped addresses
     assert fused_dev(s=A[2] + 8) == dd.ERR_INVALID_ARG
+
+
+# ------------------------------------------------------------ many tensors --
+def multi(T=3, W=4, gdtype=dd.DT_F32, ns=None, mode=dd.AGG_FP32, k=24, grads=None,
+          params=None, ms=None, vs=None, p16s="default", h="default"):
+    """Tensor j's buffers at A[...]-style fake addresses far apart."""
+    base = lambda j, i: 0x20_0000_0000 + (j * 16 + i) * 0x1_0000_0000
+    ns = [N] * T if ns is None else ns
+    grads = [base(j, w) for j in range(T) for w in range(W)] if grads is None else grads
+    params = [base(j, 12) for j in range(T)] if params is None else params
+    ms = [base(j, 13) for j in range(T)] if ms is None else ms
+    vs = [base(j, 14) for j in range(T)] if vs is None else vs
+    p16s = [base(j, 15) for j in range(T)] if p16s == "default" else p16s
+    h = hp() if h == "default" else h
+    return dd.raw_aggregate_adam_multi(grads, W, gdtype, T, ns, mode, k, params, ms, vs, p16s,
+                                       h, 0)
+
+
+def test_multi_argument_checks():
+    assert multi(T=-1, ns=[]) == dd.ERR_INVALID_ARG
+    assert multi(T=65537, ns=[0] * 65537) == dd.ERR_INVALID_ARG
+    assert multi(W=0, grads=[]) == dd.ERR_INVALID_ARG
+    assert multi(gdtype=7) == dd.ERR_UNSUPPORTED
+    assert multi(gdtype=dd.DT_I32) == dd.ERR_UNSUPPORTED           # int32 only in fixed mode
+    assert multi(mode=dd.AGG_FIXED, k=31) == dd.ERR_INVALID_ARG
+    assert multi(h=hp(step=0)) == dd.ERR_INVALID_ARG
+    assert multi(h=None) == dd.ERR_INVALID_ARG
+    assert multi(ns=[N, -1, N]) == dd.ERR_INVALID_ARG
+    assert multi(ns=[N, 2**56 + 1, N]) == dd.ERR_INVALID_ARG
+    g = [0x20_0000_0000 + i * 0x1_0000_0000 for i in range(12)]
+    g[5] = 0
+    assert multi(grads=g) == dd.ERR_INVALID_ARG                     # NULL contribution
+    assert multi(vs=[0x50_0000_0000, 0, 0x51_0000_0000]) == dd.ERR_INVALID_ARG
+    # empty lists and all-empty tensors need no pointers
+    assert multi(T=0, ns=[], grads=[], params=[], ms=[], vs=[], p16s=None) == dd.OK
+    assert dd.raw_aggregate_adam_multi(None, 4, dd.DT_F32, 2, [0, 0], dd.AGG_FP32, 0, None, None,
+                                       None, None, hp(), 0) == dd.OK
+    # a NULL entry is fine for an empty tensor; a NULL array is not for a full one
+    assert multi(ns=[N, 0, N], vs=[0x50_0000_0000, 0, 0x51_0000_0000]) == dd.ERR_INVALID_ARG  # fake, unmapped
+
+
+def test_multi_aliasing_across_tensors():
+    T, W = 3, 4
+    base = lambda j, i: 0x20_0000_0000 + (j * 16 + i) * 0x1_0000_0000
+    # tensor 1's weight array inside tensor 2's third contribution
+    assert multi(params=[base(0, 12), base(2, 2) + 64, base(2, 12)]) == dd.ERR_ALIAS
+    # two tensors sharing one moment array
+    assert multi(ms=[base(0, 13), base(0, 13), base(2, 13)]) == dd.ERR_ALIAS
+    # a bf16 copy straddling the end of another tensor's v
+    assert multi(p16s=[base(0, 15), base(0, 14) + 4 * N - 2, base(2, 15)]) == dd.ERR_ALIAS
+    # contributions shared between tensors are legal (read only); the call
+    # then fails later, on the fake unmapped addresses
+    g = [base(j, w) for j in range(T) for w in range(W)]
+    g[4] = g[0]
+    assert multi(grads=g) == dd.ERR_INVALID_ARG
+
+
+def test_multi_takes_exactly_one_source_of_step_constants():
+    base = 0x70_0000_0000
+
+    def call(h, sc):
+        return dd.raw_aggregate_adam_multi(
+            [0x20_0000_0000 + i * 0x1_0000_0000 for i in range(8)], 4, dd.DT_F32, 2, [N, N],
+            dd.AGG_FP32, 0, [0x30_0000_0000, 0x31_0000_0000], [0x32_0000_0000, 0x33_0000_0000],
+            [0x34_0000_0000, 0x35_0000_0000], None, h, 0, scalars=sc)
+    assert call(hp(), base) == dd.ERR_INVALID_ARG        # both
+    assert call(None, 0) == dd.ERR_INVALID_ARG           # neither
+    assert call(None, base + 2) == dd.ERR_INVALID_ARG    # misaligned
+    assert call(None, 0x34_0000_0000 + 8) == dd.ERR_ALIAS  # inside an output
+    # a valid combination gets as far as the (fake, unmapped) addresses
+    assert call(None, base) == dd.ERR_INVALID_ARG
+    assert call(hp(), 0) == dd.ERR_INVALID_ARG

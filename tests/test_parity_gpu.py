@@ -1055,3 +1055,150 @@ def test_shard_falls_back_to_the_caching_allocator(monkeypatch):
         t_.cuda.synchronize()
         assert_parity({"p": to_host(sh.param), "m": to_host(sh.m), "v": to_host(sh.v),
                        "p16": to_host(sh.param_bf16)}, want, "caching-allocator shard")
+
+
+# ------------------------------------------------------------ many tensors --
+def _multi_tensors(rng, T, W, gdtype, unrelated=False, sizes=None, seed=800):
+    """T tensors, each in buffers of its own at random element offsets
+    (one offset per tensor, or one per array), with host copies."""
+    tensors, host = [], []
+    choices = [0, 1, 2, 3, 4, 5, 63, 255, 256, 257, 1000, 4099, 20_001, 65_541]
+    for j in range(T):
+        n = sizes[j] if sizes is not None else int(rng.choice(choices))
+        gt = "f32" if gdtype == "i32" else gdtype
+        gs = synth.host_grads(seed + j, 1, W, n, 1e-4, gdtype=gt, outlier_frac=0.01,
+                              outlier_scale=100.0)
+        if gdtype == "i32":
+            gs = [oracle.quantize_array(g, 24) for g in gs]
+        p, m, v = synth.host_state(seed + j, n, mv_sigma=1e-4)
+        off = [int(x) for x in rng.integers(0, 300, W + 4)] if unrelated else \
+            [int(rng.integers(0, 300))] * (W + 4)
+        dg = [to_dev(g, off[w]) for w, g in enumerate(gs)]
+        dp, dm, dv = to_dev(p, off[W]), to_dev(m, off[W + 1]), to_dev(v, off[W + 2])
+        d16 = to_dev(np.zeros(n, np.uint16), off[W + 3])
+        tensors.append((dg, dp, dm, dv, d16))
+        host.append((gs, p, m, v))
+    return tensors, host
+
+
+@pytest.mark.parametrize("gdtype,mode", [("f32", "fp32"), ("bf16", "fp32"), ("f32", "fixed"),
+                                         ("bf16", "fixed"), ("i32", "fixed")])
+@pytest.mark.parametrize("W", [1, 3, 8, 13])
+def test_multi_tensor_call_matches_oracle(gdtype, mode, W):
+    """disdp_aggregate_adam_multi over 40 tensors of mixed sizes (empty ones
+    included), each in buffers of its own at common or unrelated offsets
+    (bf16 arrays of both parities take the single-tensor element path):
+    every tensor against the oracle."""
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    rng = np.random.default_rng(1000 + W)
+    for unrelated in (False, True):
+        tensors, host = _multi_tensors(rng, 40, W, gdtype, unrelated=unrelated)
+        dd.aggregate_adam_multi(tensors, lr=HP["lr"], beta1=HP["beta1"], beta2=HP["beta2"],
+                                eps=HP["eps"], weight_decay=HP["wd"], step=3, mode=mode,
+                                frac_bits=24)
+        t_.cuda.synchronize()
+        for j, ((dg, dp, dm, dv, d16), (gs, p, m, v)) in enumerate(zip(tensors, host)):
+            want = oracle.fused(gs, p, m, v, mode=oracle.AGG_FIXED if mode == "fixed"
+                                else oracle.AGG_FP32, frac_bits=24, t=3, **HP)
+            assert_parity({"p": to_host(dp), "m": to_host(dm), "v": to_host(dv),
+                           "p16": to_host(d16)}, want,
+                          _label(j=j, n=p.size, unrelated=unrelated))
+
+
+@pytest.mark.parametrize("W,T", [(8, 150), (64, 21), (2, 60)])
+def test_multi_tensor_call_equals_one_call_per_tensor(W, T):
+    """Across many batches (W = 8: 26 tensors per launch; W = 64: 4), with
+    and without bf16 copies: the multi-tensor call gives the bits of one
+    disdp_aggregate_adam per tensor."""
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    rng = np.random.default_rng(2000 + W)
+    sizes = [int(x) for x in rng.integers(0, 30_000, T)]
+    a, _ = _multi_tensors(rng, T, W, "f32", sizes=sizes, seed=900)
+    b = [([g.clone() for g in dg], dp.clone(), dm.clone(), dv.clone(), d16.clone())
+         for dg, dp, dm, dv, d16 in a]
+    for copies in (True, False):
+        kw = dict(lr=HP["lr"], beta1=HP["beta1"], beta2=HP["beta2"], eps=HP["eps"],
+                  weight_decay=HP["wd"], step=5 if copies else 6)
+        dd.aggregate_adam_multi([(g, p, m, v, c if copies else None) for g, p, m, v, c in a],
+                                **kw)
+        for g, p, m, v, c in b:
+            dd.aggregate_adam(g, p, m, v, c if copies else None, **kw)
+        t_.cuda.synchronize()
+        for j, (x, y) in enumerate(zip(a, b)):
+            for u, w in zip(x[1:], y[1:]):
+                assert t_.equal(u, w), _label(j=j, n=sizes[j], copies=copies)
+
+
+def test_multi_tensor_call_captured_in_a_hip_graph():
+    """The multi-tensor call enqueues kernel launches only: captured once,
+    replayed three times with eager work between, it equals the same call
+    made eagerly on copies of the state."""
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    rng = np.random.default_rng(77)
+    a, _ = _multi_tensors(rng, 60, 8, "f32", seed=950)
+    b = [(dg, dp.clone(), dm.clone(), dv.clone(), d16.clone()) for dg, dp, dm, dv, d16 in a]
+    kw = dict(lr=HP["lr"], beta1=HP["beta1"], beta2=HP["beta2"], eps=HP["eps"],
+              weight_decay=HP["wd"], step=2)
+    t_.cuda.synchronize()
+    side = t_.cuda.Stream()
+    graph = t_.cuda.CUDAGraph()
+    with t_.cuda.graph(graph, stream=side):
+        dd.aggregate_adam_multi(a, **kw)
+    t_.cuda.synchronize()
+    other = t_.zeros(1 << 20, device="cuda")
+    for r in range(3):
+        graph.replay()
+        dd.aggregate_adam_multi(b, **kw)
+        t_.cuda.synchronize()
+        other.add_(1.0)
+        t_.cuda.synchronize()
+        for j, (x, y) in enumerate(zip(a, b)):
+            for u, w in zip(x[1:], y[1:]):
+                assert t_.equal(u, w), _label(replay=r, j=j)
+    del graph
+
+
+def test_multi_tensor_graph_serves_every_step():
+    """The multi-tensor call with the step's constants in device memory,
+    captured once with the copy node that refreshes them, replayed for four
+    steps with fresh contributions: every tensor against the oracle each
+    step."""
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    rng = np.random.default_rng(88)
+    W = 5
+    tensors, host = _multi_tensors(rng, 30, W, "f32", seed=970)
+    kw = dict(lr=HP["lr"], beta1=HP["beta1"], beta2=HP["beta2"], eps=HP["eps"],
+              weight_decay=HP["wd"])
+    hst = t_.zeros(10, dtype=t_.float32, pin_memory=True)
+    dev = t_.zeros(10, dtype=t_.float32, device="cuda")
+    t_.cuda.synchronize()
+    side = t_.cuda.Stream()
+    graph = t_.cuda.CUDAGraph()
+    with t_.cuda.graph(graph, stream=side):
+        dev.copy_(hst, non_blocking=True)
+        dd.aggregate_adam_multi(tensors, scalars=dev)
+    t_.cuda.synchronize()
+    state = [(p, m, v) for _, p, m, v in host]
+    for t in range(1, 5):
+        grads = []
+        for j, (dg, *_rest) in enumerate(tensors):
+            n = dg[0].numel()
+            gs = synth.host_grads(5000 + 31 * t + j, t, W, n, 1e-4)
+            for d, g in zip(dg, gs):
+                d.copy_(t_.from_numpy(g))
+            grads.append(gs)
+        hst.copy_(t_.frombuffer(bytearray(dd.step_scalars(step=t, **kw)), dtype=t_.float32))
+        t_.cuda.synchronize()
+        graph.replay()
+        t_.cuda.synchronize()
+        for j, ((dg, dp, dm, dv, d16), gs) in enumerate(zip(tensors, grads)):
+            p, m, v = state[j]
+            want = oracle.fused(gs, p, m, v, t=t, **HP)
+            assert_parity({"p": to_host(dp), "m": to_host(dm), "v": to_host(dv),
+                           "p16": to_host(d16)}, want, _label(step=t, j=j))
+            state[j] = (want["p"], want["m"], want["v"])
+    del graph
