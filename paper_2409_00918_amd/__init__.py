@@ -25,10 +25,10 @@ call raises.
 """
 from __future__ import annotations
 
-import atexit
 import ctypes
 import os
 import sys
+import threading
 from typing import Optional, Sequence
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
@@ -468,14 +468,6 @@ def shard_layout(n: int, W: int, gdtype="f32", *, bf16_copy=True, agg_f32=False,
 
 _HIP_DEVICE_MALLOC_CONTIGUOUS = 0x4    # hipDeviceMallocContiguous
 _hip = None
-_exiting = False
-
-
-@atexit.register
-def _mark_exiting() -> None:
-    # device memory still held at exit goes with the process
-    global _exiting
-    _exiting = True
 
 
 def _hip_runtime() -> ctypes.CDLL:
@@ -488,18 +480,19 @@ def _hip_runtime() -> ctypes.CDLL:
         L.hipExtMallocWithFlags.restype = ctypes.c_int
         L.hipExtMallocWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_size_t,
                                             ctypes.c_uint]
-        L.hipFree.restype = ctypes.c_int
-        L.hipFree.argtypes = [ctypes.c_void_p]
         L.hipGetLastError.restype = ctypes.c_int
         _hip = L
     return _hip
 
 
-class _ContiguousSlab:
+class _ContiguousBlock:
     """One physically contiguous device allocation (hipExtMallocWithFlags
-    with hipDeviceMallocContiguous), handed to torch through
-    __cuda_array_interface__: torch keeps this object alive while any view
-    of the memory exists, and the memory is freed with it."""
+    with hipDeviceMallocContiguous).  Blocks are never freed while the
+    process runs: on MI355X, memory that torch's caching allocator later
+    placed in the address range of a freed contiguous block was read back
+    stale or zero by kernels that ran after a synchronised copy into it.
+    A released block returns to the pool and serves the next request that
+    fits."""
 
     def __init__(self, nbytes: int, device_index: int):
         torch = _torch()
@@ -513,35 +506,78 @@ class _ContiguousSlab:
             hip.hipGetLastError()           # clear the recorded error
             raise MemoryError(f"no physically contiguous block of {nbytes} bytes "
                               f"(HIP error {rc})")
+        self.nbytes = nbytes
+        self.device_index = device_index
+        self.leased = False
+
+
+_blocks = []                       # every contiguous block of this process
+_blocks_lock = threading.RLock()   # reentrant: a lease may be collected while held
+
+
+class _Lease:
+    """The owner torch holds for a tensor over (a prefix of) one block,
+    through __cuda_array_interface__: torch keeps it alive while any view
+    exists, and collecting it hands the block back to the pool."""
+
+    def __init__(self, block: _ContiguousBlock, nbytes: int):
+        self.block = block
         self.__cuda_array_interface__ = {"shape": (nbytes,), "typestr": "|u1",
-                                         "data": (self.ptr, False), "version": 2}
+                                         "data": (block.ptr, False), "version": 2}
 
     def __del__(self):
-        if self.ptr and not _exiting:
-            _hip_runtime().hipFree(self.ptr)
-        self.ptr = 0
+        self.block.leased = False
+
+
+def _lease_block(nbytes: int, device_index: int):
+    """The smallest free pooled block of at least `nbytes` on the device,
+    else a new block; None when the runtime has none."""
+    with _blocks_lock:
+        fits = [b for b in _blocks if not b.leased and b.device_index == device_index
+                and b.nbytes >= nbytes]
+        if fits:
+            block = min(fits, key=lambda b: b.nbytes)
+        else:
+            try:
+                block = _ContiguousBlock(nbytes, device_index)
+            except MemoryError:
+                return None
+            _blocks.append(block)
+        block.leased = True
+        return block
+
+
+def contiguous_pool(device="cuda"):
+    """(bytes held, bytes leased) by the contiguous-block pool on a device."""
+    torch = _torch()
+    dev = torch.device(device)
+    idx = dev.index if dev.index is not None else torch.cuda.current_device()
+    with _blocks_lock:
+        mine = [b for b in _blocks if b.device_index == idx]
+        return sum(b.nbytes for b in mine), sum(b.nbytes for b in mine if b.leased)
 
 
 def contiguous_bytes(nbytes: int, device="cuda"):
     """A uint8 device tensor of `nbytes` over one physically contiguous
-    allocation (freed with its last view), or None when the runtime has no
-    such block (or torch cannot wrap it)."""
+    block (pooled for the life of the process, back in the pool when the
+    last view goes), or None when the runtime has no such block (or torch
+    cannot wrap it)."""
     torch = _torch()
     dev = torch.device(device)
     idx = dev.index if dev.index is not None else torch.cuda.current_device()
-    try:
-        owner = _ContiguousSlab(nbytes, idx)
-    except MemoryError:
+    block = _lease_block(nbytes, idx)
+    if block is None:
         return None
+    owner = _Lease(block, nbytes)
     refs = sys.getrefcount(owner)
     try:
         t = torch.as_tensor(owner, device=torch.device("cuda", idx))
     except (TypeError, RuntimeError, ValueError):
-        return None
-    # the tensor must hold the owner (which frees the memory when collected)
+        return None                 # the lease goes with `owner`
+    # the tensor must hold the lease (which returns the block when collected)
     if sys.getrefcount(owner) <= refs:
         return None
-    if t.data_ptr() != owner.ptr or t.numel() != nbytes or t.dtype != torch.uint8:
+    if t.data_ptr() != block.ptr or t.numel() != nbytes or t.dtype != torch.uint8:
         return None
     return t
 

@@ -329,6 +329,94 @@ void graph_case(const char *label, int W, int gdtype, int64_t n, int mode, int k
     HIP_OK(hipStreamDestroy(s));
 }
 
+// Many tensors in separate buffers through one disdp_aggregate_adam_multi
+// call (sizes from empty to a few tiles plus ragged tails, one tensor at an
+// odd element offset), every tensor compared with the oracle.
+void multi_case(int W, int gdtype, int mode, int k)
+{
+    const char *label = "multi-tensor call";
+    hipStream_t s;
+    HIP_OK(hipStreamCreate(&s));
+    const int64_t sizes[] = {0, 1, 3, 4, 257, 1000, 4099, 65541, 7, 300007, 2, 256};
+    const int T = static_cast<int>(sizeof sizes / sizeof sizes[0]);
+    const size_t eb = gdtype == DISDP_DT_BF16 ? 2 : 4;
+    std::vector<void *> allocs;
+    std::vector<const void *> g(static_cast<size_t>(T) * W);
+    std::vector<float *> dp(T), dm(T), dv(T);
+    std::vector<uint16_t *> d16(T);
+    std::vector<std::vector<float>> p(T), m(T), v(T);
+    std::vector<HostGrads> hg;
+    for (int j = 0; j < T; ++j) {
+        const int64_t n = sizes[j];
+        const int off = j == 5 ? 3 : 0;   // tensor 5 starts 3 elements into its buffers
+        hg.emplace_back(W, gdtype, n, 3000 + j, 1e-4f);
+        for (int w = 0; w < W; ++w) {
+            void *b;
+            HIP_OK(hipMalloc(&b, (n + off + 1) * eb));
+            allocs.push_back(b);
+            char *q = static_cast<char *>(b) + off * eb;
+            HIP_OK(hipMemcpy(q, hg[j].ptr(w), n * eb, hipMemcpyDefault));
+            g[static_cast<size_t>(j) * W + w] = q;
+        }
+        p[j].resize(n);
+        m[j].resize(n);
+        v[j].resize(n);
+        for (int64_t i = 0; i < n; ++i) {
+            p[j][i] = draw(7201 + j, i, 0.02f);
+            m[j][i] = draw(7301 + j, i, 1e-4f);
+            const float r = draw(7401 + j, i, 1e-4f);
+            v[j][i] = r * r;
+        }
+        float **outs[] = {&dp[j], &dm[j], &dv[j]};
+        std::vector<float> *src[] = {&p[j], &m[j], &v[j]};
+        for (int a = 0; a < 3; ++a) {
+            void *b;
+            HIP_OK(hipMalloc(&b, (n + off + 1) * 4));
+            allocs.push_back(b);
+            *outs[a] = static_cast<float *>(b) + off;
+            HIP_OK(hipMemcpy(*outs[a], src[a]->data(), n * 4, hipMemcpyDefault));
+        }
+        void *b;
+        HIP_OK(hipMalloc(&b, (n + off + 1) * 2));
+        allocs.push_back(b);
+        d16[j] = static_cast<uint16_t *>(b) + off;
+    }
+    Hp h;
+    const disdp_adamw_hparams_t hp = hparams(h, 4);
+    expect(disdp_aggregate_adam_multi(g.data(), W, static_cast<disdp_dtype_t>(gdtype), T, sizes,
+                                      static_cast<disdp_agg_mode_t>(mode), k, dp.data(),
+                                      dm.data(), dv.data(), d16.data(), &hp, nullptr, s),
+           DISDP_OK, label);
+    HIP_OK(hipStreamSynchronize(s));
+    bool ok = true;
+    for (int j = 0; j < T && ok; ++j) {
+        const int64_t n = sizes[j];
+        if (n == 0)
+            continue;
+        std::vector<const void *> hp_ptrs(W);
+        for (int w = 0; w < W; ++w)
+            hp_ptrs[w] = hg[j].ptr(w);
+        std::vector<uint16_t> want16(n), got16(n);
+        std::vector<float> gp(n), gm(n), gv(n);
+        oracle_fused(hp_ptrs.data(), W, gdtype, n, mode, k, p[j].data(), m[j].data(),
+                     v[j].data(), want16.data(), nullptr, nullptr, h.lr, h.b1, h.b2, h.eps, h.wd,
+                     4, 1.0f);
+        HIP_OK(hipMemcpy(gp.data(), dp[j], n * 4, hipMemcpyDefault));
+        HIP_OK(hipMemcpy(gm.data(), dm[j], n * 4, hipMemcpyDefault));
+        HIP_OK(hipMemcpy(gv.data(), dv[j], n * 4, hipMemcpyDefault));
+        HIP_OK(hipMemcpy(got16.data(), d16[j], n * 2, hipMemcpyDefault));
+        ok = same(gp.data(), p[j].data(), n * 4, "p", label) && ok;
+        ok = same(gm.data(), m[j].data(), n * 4, "m", label) && ok;
+        ok = same(gv.data(), v[j].data(), n * 4, "v", label) && ok;
+        ok = same(got16.data(), want16.data(), n * 2, "p16", label) && ok;
+    }
+    std::printf("%s %s: T=%d W=%d gdtype=%d mode=%d\n", ok ? "ok" : "FAIL", label, T, W, gdtype,
+                mode);
+    for (void *b : allocs)
+        HIP_OK(hipFree(b));
+    HIP_OK(hipStreamDestroy(s));
+}
+
 // The worker-side conversion, then the aggregation of int32 contributions,
 // against the oracle's conversion and fixed-point aggregation of the floats.
 void quantize_case(int W, int64_t n, int k)
@@ -570,6 +658,10 @@ int main(int argc, char **argv)
     graph_case("graph replay fp32 W=6", 6, DISDP_DT_F32, 500009, DISDP_AGG_FP32, 0, 4);
     std::fflush(stdout);
     graph_case("graph replay fixed bf16 W=13", 13, DISDP_DT_BF16, 200003, DISDP_AGG_FIXED, 24, 3);
+    std::fflush(stdout);
+    multi_case(4, DISDP_DT_F32, DISDP_AGG_FP32, 0);
+    std::fflush(stdout);
+    multi_case(9, DISDP_DT_BF16, DISDP_AGG_FIXED, 24);
     std::fflush(stdout);
     quantize_case(6, 500009, 24);
     std::fflush(stdout);

@@ -995,8 +995,9 @@ def test_fused_on_a_shard_placed_by_the_layout_planner(W, gdtype, mode):
 def test_contiguous_shard_slab_lifetime():
     """allocate_shard's physically contiguous slab: every view sits at the
     planner's offset inside it, the memory stays valid while any view is
-    alive after the Shard object is gone, and is returned to the device when
-    the last view goes."""
+    alive after the Shard object is gone, and when the last view goes the
+    block returns to the process's pool (never to the device) and serves
+    the next shard that fits."""
     import gc
     import paper_2409_00918_amd as dd
     t_ = torch()
@@ -1004,28 +1005,43 @@ def test_contiguous_shard_slab_lifetime():
     gc.collect()
     t_.cuda.synchronize()
     free0, _ = t_.cuda.mem_get_info()
+    held0, leased0 = dd.contiguous_pool()
     sh = dd.allocate_shard(n, W, "f32")
     assert sh.contiguous, "the runtime refused a physically contiguous slab"
     offs, total = dd.shard_layout(n, W, "f32")
     base = sh.slab.data_ptr()
     for i, x in enumerate(sh.grads + [sh.param, sh.m, sh.v, sh.param_bf16]):
         assert x.data_ptr() == base + offs[i], i
+    held1, leased1 = dd.contiguous_pool()
+    assert leased1 - leased0 >= total
     slack = 64 << 20                 # device-wide free-memory accounting is not exact
-    free1, _ = t_.cuda.mem_get_info()
-    assert free0 - free1 >= total - slack
+    if held1 > held0:                # a new block, not one from the pool
+        free1, _ = t_.cuda.mem_get_info()
+        assert free0 - free1 >= total - slack
     keep = sh.v
     keep.fill_(1.5)
     del sh, x
     gc.collect()
     t_.cuda.synchronize()
-    free2, _ = t_.cuda.mem_get_info()
-    assert free0 - free2 >= total - slack         # still held by the view
+    assert dd.contiguous_pool()[1] == leased1                  # still held by the view
     assert bool((keep[-1000:] == 1.5).all()) and bool((keep[:1000] == 1.5).all())
     del keep
     gc.collect()
     t_.cuda.synchronize()
-    free3, _ = t_.cuda.mem_get_info()
-    assert free0 - free3 < total // 2             # returned
+    held2, leased2 = dd.contiguous_pool()
+    assert leased2 == leased0 and held2 == held1               # back in the pool
+    free2, _ = t_.cuda.mem_get_info()
+    assert free0 - free2 >= (held1 - held0) - slack            # not back on the device
+    # the next shard that fits takes the pooled block; a second one at the
+    # same time gets a block of its own
+    a = dd.allocate_shard(n - 1000, W, "f32")
+    assert a.contiguous and dd.contiguous_pool()[0] == held2   # no new block
+    b = dd.allocate_shard(n - 2000, W, "f32")
+    assert b.contiguous and b.slab.data_ptr() != a.slab.data_ptr()
+    assert dd.contiguous_pool()[1] >= leased0 + a.slab.numel() + b.slab.numel()
+    del a, b
+    gc.collect()
+    assert dd.contiguous_pool()[1] == leased0
 
 
 def test_shard_falls_back_to_the_caching_allocator(monkeypatch):
@@ -1042,7 +1058,7 @@ def test_shard_falls_back_to_the_caching_allocator(monkeypatch):
     monkeypatch.setattr(dd, "contiguous_bytes", lambda nbytes, device="cuda": None)
     shards.append(dd.allocate_shard(n, W, "f32"))
     offs, _ = dd.shard_layout(n, W, "f32")
-    for sh in shards:
+    for which, sh in enumerate(shards):
         assert not sh.contiguous
         assert sh.param.data_ptr() == sh.slab.data_ptr() + offs[W]
         for dst, src in zip(sh.grads, gs):
@@ -1053,8 +1069,19 @@ def test_shard_falls_back_to_the_caching_allocator(monkeypatch):
                           beta1=HP["beta1"], beta2=HP["beta2"], eps=HP["eps"],
                           weight_decay=HP["wd"], step=2)
         t_.cuda.synchronize()
-        assert_parity({"p": to_host(sh.param), "m": to_host(sh.m), "v": to_host(sh.v),
-                       "p16": to_host(sh.param_bf16)}, want, "caching-allocator shard")
+        got = {"p": to_host(sh.param), "m": to_host(sh.m), "v": to_host(sh.v),
+               "p16": to_host(sh.param_bf16)}
+        diag = []
+        for k, inp in (("p", p), ("m", m), ("v", v)):
+            d = np.flatnonzero(bits(got[k]) != bits(want[k]))
+            if d.size:
+                runs = int(np.count_nonzero(np.diff(d) != 1)) + 1
+                unwritten = int(np.count_nonzero(bits(got[k][d]) == bits(inp[d])))
+                diag.append(f"{k}: {d.size} differ in {runs} runs, [{d.min()}, {d.max()}], "
+                            f"{unwritten} still the input, got {got[k][d[:3]]} "
+                            f"want {want[k][d[:3]]}")
+        assert_parity(got, want, f"caching-allocator shard {which} at "
+                                 f"{sh.slab.data_ptr():#x}: {'; '.join(diag)}")
 
 
 # ------------------------------------------------------------ many tensors --
