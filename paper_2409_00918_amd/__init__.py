@@ -531,12 +531,15 @@ class _Lease:
 
 def _lease_block(nbytes: int, device_index: int):
     """The smallest free pooled block of at least `nbytes` on the device,
-    else a new block; None when the runtime has none."""
+    else a new block; None when the runtime has none.  A pooled block is
+    handed out again only once the device has finished the work already
+    queued on it, from any stream (the wait hipFree would have made)."""
     with _blocks_lock:
         fits = [b for b in _blocks if not b.leased and b.device_index == device_index
                 and b.nbytes >= nbytes]
         if fits:
             block = min(fits, key=lambda b: b.nbytes)
+            _torch().cuda.synchronize(device_index)
         else:
             try:
                 block = _ContiguousBlock(nbytes, device_index)
