@@ -551,13 +551,15 @@ def _lease_block(nbytes: int, device_index: int):
 
 
 def contiguous_pool(device="cuda"):
-    """(bytes held, bytes leased) by the contiguous-block pool on a device."""
+    """(bytes held, bytes leased, largest idle block) of the contiguous-block
+    pool on a device."""
     torch = _torch()
     dev = torch.device(device)
     idx = dev.index if dev.index is not None else torch.cuda.current_device()
     with _blocks_lock:
         mine = [b for b in _blocks if b.device_index == idx]
-        return sum(b.nbytes for b in mine), sum(b.nbytes for b in mine if b.leased)
+        return (sum(b.nbytes for b in mine), sum(b.nbytes for b in mine if b.leased),
+                max((b.nbytes for b in mine if not b.leased), default=0))
 
 
 def contiguous_bytes(nbytes: int, device="cuda"):

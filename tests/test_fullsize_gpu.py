@@ -40,10 +40,74 @@ def sample_indices(n, seed):
     return idx[(idx >= 0) & (idx < n)].astype(np.int64)
 
 
-def bytes_needed(wl):
+def shard_bytes(wl):
     gb = 2 if wl.gdtype == "bf16" else 4
-    n = wl.n
-    return n * (wl.W * gb + 12 + 2 + (4 if wl.mode == "fixed" else 0)) + n * 4 * 3
+    return wl.n * (wl.W * gb + 12 + 2 + (4 if wl.mode == "fixed" else 0))
+
+
+def bytes_needed(wl):
+    return shard_bytes(wl) + wl.n * 4 * 3
+
+
+def room_for(wl):
+    """Device memory a shard test can use: what is free, plus an idle block
+    of the contiguous pool large enough to hold the shard (a shard released
+    by an earlier test stays in the pool and serves the next one)."""
+    import paper_2409_00918_amd as dd
+    free, _ = torch().cuda.mem_get_info()
+    idle = dd.contiguous_pool()[2]
+    return free + (idle if idle >= shard_bytes(wl) else 0)
+
+
+def test_grids_beyond_2_to_the_32_lanes():
+    """A shard of 2^34 + 12,345 elements needs more one-tile blocks (and
+    more quantize lanes) than one dispatch counts (2^32 - 1 work-items):
+    the library clamps its grids and the kernels walk the rest grid-stride.
+    disdp_aggregate of one bf16 contribution in fp32 mode returns every
+    element widened, checked over all of them (arbitrary bit patterns, NaNs
+    included: no arithmetic touches them); disdp_quantize of the same array
+    matches the oracle on sampled elements, including those the clamped grid
+    reaches on its second pass and the last ones."""
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    n = (1 << 34) + 12_345
+    free, _ = t_.cuda.mem_get_info()
+    if n * 6 + (1 << 31) > 0.92 * free:
+        pytest.skip(f"needs {n * 6 / 2**30:.0f} GiB, {free / 2**30:.0f} free")
+    chunk = 1 << 28
+    print(f"[fullsize] 2^34+ n={n} fill", flush=True)
+    g = t_.empty(n, dtype=t_.int16, device="cuda")
+    gen = t_.Generator(device="cuda")
+    gen.manual_seed(34)
+    for s in range(0, n, chunk):
+        e = min(n, s + chunk)
+        g[s:e] = t_.randint(-32768, 32768, (e - s,), dtype=t_.int32, device="cuda",
+                            generator=gen).to(t_.int16)
+    agg = t_.empty(n, dtype=t_.float32, device="cuda")
+    print("[fullsize] 2^34+ aggregate", flush=True)
+    dd.aggregate([g], mode="fp32", agg_out_f32=agg)
+    t_.cuda.synchronize()
+    for s in range(0, n, chunk):
+        e = min(n, s + chunk)
+        same = t_.equal(agg[s:e].view(t_.int32), g[s:e].to(t_.int32) << 16)
+        assert same, f"aggregate differs in [{s}, {e})"
+    del agg
+    out = t_.empty(n, dtype=t_.int32, device="cuda")
+    print("[fullsize] 2^34+ quantize", flush=True)
+    dd.quantize(g, out, frac_bits=24)
+    t_.cuda.synchronize()
+    # one 64-lane block per 256 elements, at most (2^32 - 1) // 64 blocks:
+    # the first pass of the clamped grid ends here
+    first_pass = ((2**32 - 1) // 64) * 64 * 4
+    idx = np.unique(np.concatenate([sample_indices(n, 34),
+                                    np.arange(first_pass - 300, first_pass + 300)]))
+    ti = t_.from_numpy(idx).cuda()
+    gh = g[ti].cpu().numpy().view(np.uint16)
+    want = oracle.quantize_array(gh, 24)
+    got = out[ti].cpu().numpy()
+    assert np.array_equal(got, want)
+    del out, g
+    t_.cuda.empty_cache()
 
 
 @pytest.mark.parametrize("name", ["opt7b_shard8_w8_f32", "opt13b_shard16_w16_bf16",
@@ -52,7 +116,7 @@ def test_full_size_shard_sampled_parity(name):
     import paper_2409_00918_amd as dd
     t_ = torch()
     wl = synth.WORKLOADS[name]
-    free, _ = t_.cuda.mem_get_info()
+    free = room_for(wl)
     if bytes_needed(wl) > 0.92 * free:
         pytest.skip(f"{name} needs {bytes_needed(wl) / 2**30:.0f} GiB, {free / 2**30:.0f} free")
     n, W = wl.n, wl.W
@@ -111,7 +175,7 @@ def test_full_size_trajectory_of_40_steps():
     import paper_2409_00918_amd as dd
     t_ = torch()
     wl = synth.WORKLOADS["opt7b_shard8_w8_f32"]
-    free, _ = t_.cuda.mem_get_info()
+    free = room_for(wl)
     if bytes_needed(wl) > 0.92 * free:
         pytest.skip("not enough device memory")
     n, W = wl.n, wl.W
@@ -143,57 +207,6 @@ def test_full_size_trajectory_of_40_steps():
         t_.cuda.empty_cache()
 
 
-def test_grids_beyond_2_to_the_32_lanes():
-    """A shard of 2^34 + 12,345 elements needs more one-tile blocks (and
-    more quantize lanes) than one dispatch counts (2^32 - 1 work-items):
-    the library clamps its grids and the kernels walk the rest grid-stride.
-    disdp_aggregate of one bf16 contribution in fp32 mode returns every
-    element widened, checked over all of them (arbitrary bit patterns, NaNs
-    included: no arithmetic touches them); disdp_quantize of the same array
-    matches the oracle on sampled elements, including those the clamped grid
-    reaches on its second pass and the last ones."""
-    import paper_2409_00918_amd as dd
-    t_ = torch()
-    n = (1 << 34) + 12_345
-    free, _ = t_.cuda.mem_get_info()
-    if n * 6 + (1 << 31) > 0.92 * free:
-        pytest.skip(f"needs {n * 6 / 2**30:.0f} GiB, {free / 2**30:.0f} free")
-    chunk = 1 << 28
-    print(f"[fullsize] 2^34+ n={n} fill", flush=True)
-    g = t_.empty(n, dtype=t_.int16, device="cuda")
-    gen = t_.Generator(device="cuda")
-    gen.manual_seed(34)
-    for s in range(0, n, chunk):
-        e = min(n, s + chunk)
-        g[s:e] = t_.randint(-32768, 32768, (e - s,), dtype=t_.int32, device="cuda",
-                            generator=gen).to(t_.int16)
-    agg = t_.empty(n, dtype=t_.float32, device="cuda")
-    print("[fullsize] 2^34+ aggregate", flush=True)
-    dd.aggregate([g], mode="fp32", agg_out_f32=agg)
-    t_.cuda.synchronize()
-    for s in range(0, n, chunk):
-        e = min(n, s + chunk)
-        same = t_.equal(agg[s:e].view(t_.int32), g[s:e].to(t_.int32) << 16)
-        assert same, f"aggregate differs in [{s}, {e})"
-    del agg
-    out = t_.empty(n, dtype=t_.int32, device="cuda")
-    print("[fullsize] 2^34+ quantize", flush=True)
-    dd.quantize(g, out, frac_bits=24)
-    t_.cuda.synchronize()
-    # one 64-lane block per 256 elements, at most (2^32 - 1) // 64 blocks:
-    # the first pass of the clamped grid ends here
-    first_pass = ((2**32 - 1) // 64) * 64 * 4
-    idx = np.unique(np.concatenate([sample_indices(n, 34),
-                                    np.arange(first_pass - 300, first_pass + 300)]))
-    ti = t_.from_numpy(idx).cuda()
-    gh = g[ti].cpu().numpy().view(np.uint16)
-    want = oracle.quantize_array(gh, 24)
-    got = out[ti].cpu().numpy()
-    assert np.array_equal(got, want)
-    del out, g
-    t_.cuda.empty_cache()
-
-
 def test_full_size_graph_replayed_across_steps():
     """The 7B/8 shard driven by one captured HIP graph (copy node for the
     step's constants + disdp_aggregate_adam_dev), replayed for 5 steps with
@@ -202,7 +215,7 @@ def test_full_size_graph_replayed_across_steps():
     import paper_2409_00918_amd as dd
     t_ = torch()
     wl = synth.WORKLOADS["opt7b_shard8_w8_f32"]
-    free, _ = t_.cuda.mem_get_info()
+    free = room_for(wl)
     if bytes_needed(wl) > 0.92 * free:
         pytest.skip("not enough device memory")
     n, W = wl.n, wl.W

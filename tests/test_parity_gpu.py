@@ -1005,14 +1005,14 @@ def test_contiguous_shard_slab_lifetime():
     gc.collect()
     t_.cuda.synchronize()
     free0, _ = t_.cuda.mem_get_info()
-    held0, leased0 = dd.contiguous_pool()
+    held0, leased0, _ = dd.contiguous_pool()
     sh = dd.allocate_shard(n, W, "f32")
     assert sh.contiguous, "the runtime refused a physically contiguous slab"
     offs, total = dd.shard_layout(n, W, "f32")
     base = sh.slab.data_ptr()
     for i, x in enumerate(sh.grads + [sh.param, sh.m, sh.v, sh.param_bf16]):
         assert x.data_ptr() == base + offs[i], i
-    held1, leased1 = dd.contiguous_pool()
+    held1, leased1, _ = dd.contiguous_pool()
     assert leased1 - leased0 >= total
     slack = 64 << 20                 # device-wide free-memory accounting is not exact
     if held1 > held0:                # a new block, not one from the pool
@@ -1028,8 +1028,8 @@ def test_contiguous_shard_slab_lifetime():
     del keep
     gc.collect()
     t_.cuda.synchronize()
-    held2, leased2 = dd.contiguous_pool()
-    assert leased2 == leased0 and held2 == held1               # back in the pool
+    held2, leased2, idle2 = dd.contiguous_pool()
+    assert leased2 == leased0 and held2 == held1 and idle2 >= total   # back in the pool
     free2, _ = t_.cuda.mem_get_info()
     assert free0 - free2 >= (held1 - held0) - slack            # not back on the device
     # the next shard that fits takes the pooled block; a second one at the
@@ -1042,6 +1042,36 @@ def test_contiguous_shard_slab_lifetime():
     del a, b
     gc.collect()
     assert dd.contiguous_pool()[1] == leased0
+
+
+def test_pooled_block_waits_for_work_queued_on_it():
+    """A contiguous block released while fused calls on another stream still
+    write into it is leased again only after that work is done: a fill made
+    on the default stream right after the new lease survives."""
+    import gc
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    n, W = 50_000_000, 4
+    a = dd.allocate_shard(n, W, "f32")
+    assert a.contiguous, "the runtime refused a physically contiguous slab"
+    base = a.slab.data_ptr()
+    for x in a.grads + [a.param, a.m, a.v]:
+        x.fill_(0.5)
+    t_.cuda.synchronize()
+    side = t_.cuda.Stream()
+    for step in range(1, 41):          # about 15 ms of writes queued on `side`
+        dd.aggregate_adam(a.grads, a.param, a.m, a.v, a.param_bf16, lr=1e-4,
+                          beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1,
+                          step=step, stream=side)
+    del a, x
+    gc.collect()
+    b = dd.allocate_shard(n, W, "f32")
+    assert b.contiguous and b.slab.data_ptr() == base, "the pooled block was not reused"
+    b.slab.fill_(7)
+    t_.cuda.synchronize()
+    assert bool((b.slab == 7).all()), "queued work wrote into the block after its new lease"
+    del b
+    gc.collect()
 
 
 def test_shard_falls_back_to_the_caching_allocator(monkeypatch):
