@@ -572,6 +572,7 @@ def run_layers(args):
     refreshes the step's constants; (d) one disdp_aggregate_adam_multi call
     (a batch of tensors per launch); (e) that call with the constants in
     device memory, captured once as a HIP graph with its copy node."""
+    import ctypes
     import numpy as np
     import torch
     import paper_2409_00918_amd as dd
@@ -620,9 +621,10 @@ def run_layers(args):
 
     # the multi-tensor call with its host arrays built once (the library
     # still checks every pointer on every call)
-    mgrads = [g.data_ptr() for ta in tensor_args for g in ta[0]]
-    mns = [ta[1].numel() for ta in tensor_args]
-    mp, mm, mv, m16 = ([ta[i].data_ptr() for ta in tensor_args] for i in (1, 2, 3, 4))
+    mgrads = dd.host_array([g.data_ptr() for ta in tensor_args for g in ta[0]])
+    mns = dd.host_array([ta[1].numel() for ta in tensor_args], ctypes.c_int64)
+    mp, mm, mv, m16 = (dd.host_array([ta[i].data_ptr() for ta in tensor_args])
+                       for i in (1, 2, 3, 4))
 
     mgraph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(mgraph, stream=side):
@@ -650,6 +652,7 @@ def run_layers(args):
     modes = {"one_call": one, "eager_per_tensor": eager, "graph_per_tensor": replay,
              "multi_tensor_call": multi, "multi_tensor_graph": mreplay}
     res = {k: [] for k in modes}
+    host_ms = {k: [] for k in modes}
     t = 0
     for rnd in range(4 + 1):
         for name, fn in modes.items():
@@ -659,16 +662,20 @@ def run_layers(args):
                 a = torch.cuda.Event(enable_timing=True)
                 b = torch.cuda.Event(enable_timing=True)
                 a.record(s)
+                h0 = time.perf_counter()
                 fn(t)
+                h1 = time.perf_counter()
                 b.record(s)
                 torch.cuda.synchronize()
                 if rnd:                      # round 0 warms every mode up
                     res[name].append(a.elapsed_time(b))
+                    host_ms[name].append((h1 - h0) * 1e3)
     out = {}
     for name, v in res.items():
         ms = float(np.median(v))
         out[name] = {"ms_per_step": round(ms, 4), "G_params_s": round(total / ms / 1e6, 2),
-                     "TBps": round(total * 58 / ms / 1e9, 3)}
+                     "TBps": round(total * 58 / ms / 1e9, 3),
+                     "host_ms_per_step": round(float(np.median(host_ms[name])), 4)}
     print(json.dumps({"metric": "G params/s, a 7B/8 shard updated tensor by tensor",
                       "tensors": len(sizes), "elements": total,
                       "smallest_tensor": min(sizes), "largest_tensor": max(sizes),

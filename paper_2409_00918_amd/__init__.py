@@ -181,18 +181,24 @@ def raw_aggregate_adam_dev(grad_ptrs, W, gdtype, n, mode, frac_bits, param, m, v
         stream or None)
 
 
+def host_array(xs, ctype=ctypes.c_void_p):
+    """A ctypes host array of `xs` (pointers as integers, 0 = NULL; or sizes
+    with ctype=c_int64); None stays None and a ctypes array passes through,
+    so a caller repeating a call can build its arrays once."""
+    if xs is None or isinstance(xs, ctypes.Array):
+        return xs
+    return (ctype * max(1, len(xs)))(*[(x or None) if ctype is ctypes.c_void_p else x
+                                       for x in xs])
+
+
 def raw_aggregate_adam_multi(grad_ptrs, W, gdtype, T, ns, mode, frac_bits, params, ms, vs,
                              p16s, hp: Optional[AdamWHParams], stream, scalars=0) -> int:
-    """Host arrays built from Python lists of integers (None = a NULL array)."""
-    def arr(xs, ctype=ctypes.c_void_p):
-        if xs is None:
-            return None
-        return (ctype * max(1, len(xs)))(*[(x or None) if ctype is ctypes.c_void_p else x
-                                           for x in xs])
+    """Host arrays from Python lists of integers or from `host_array`
+    (None = a NULL array)."""
     return lib().disdp_aggregate_adam_multi(
-        arr(grad_ptrs), W, gdtype, T, arr(ns, ctypes.c_int64), mode, frac_bits, arr(params),
-        arr(ms), arr(vs), arr(p16s), None if hp is None else ctypes.byref(hp), scalars or None,
-        stream or None)
+        host_array(grad_ptrs), W, gdtype, T, host_array(ns, ctypes.c_int64), mode, frac_bits,
+        host_array(params), host_array(ms), host_array(vs), host_array(p16s),
+        None if hp is None else ctypes.byref(hp), scalars or None, stream or None)
 
 
 # --------------------------------------------------------- torch tensors --

@@ -9,6 +9,8 @@
 #include <cstddef>
 #include <cstdint>
 #include <cstring>
+#include <iterator>
+#include <map>
 #include <vector>
 
 #include "disdp_launch.h"
@@ -98,8 +100,11 @@ disdp::StepScalars step_scalars(const disdp_adamw_hparams_t *hp)
 // managed memory, or pinned host memory mapped for the device at the same
 // address (hipHostMalloc).  Pageable host memory and unknown addresses are
 // refused here, so they never reach a kernel.
-bool gpu_addressable(const void *p)
+// `device_memory` (when given) says whether it is device or managed memory.
+bool gpu_addressable(const void *p, bool *device_memory = nullptr)
 {
+    if (device_memory)
+        *device_memory = false;
     hipPointerAttribute_t at;
     if (hipPointerGetAttributes(&at, p) != hipSuccess) {
         (void)hipGetLastError();  // clear the error this query just recorded
@@ -109,6 +114,8 @@ bool gpu_addressable(const void *p)
     case hipMemoryTypeDevice:
     case hipMemoryTypeManaged:
     case hipMemoryTypeUnified:
+        if (device_memory)
+            *device_memory = true;
         return true;
     case hipMemoryTypeHost:
         return at.devicePointer == p;
@@ -116,6 +123,47 @@ bool gpu_addressable(const void *p)
         return false;
     }
 }
+
+// gpu_addressable over the many pointers of one call: the device (or
+// managed) allocations already confirmed in this call are remembered, and a
+// pointer inside one of them needs no further query of the runtime.  Arrays
+// carved out of a few large allocations cost one query per allocation.
+class AddressableSet {
+  public:
+    bool check(const void *p)
+    {
+        const uintptr_t a = reinterpret_cast<uintptr_t>(p);
+        if (a - last_lo_ < last_size_)
+            return true;
+        auto it = known_.upper_bound(a);  // first allocation starting above a
+        if (it != known_.begin() && a - std::prev(it)->first < std::prev(it)->second) {
+            last_lo_ = std::prev(it)->first;
+            last_size_ = std::prev(it)->second;
+            return true;
+        }
+        bool device_memory = false;
+        if (!gpu_addressable(p, &device_memory))
+            return false;
+        if (device_memory) {
+            hipDeviceptr_t base = nullptr;
+            size_t size = 0;
+            if (hipMemGetAddressRange(&base, &size, const_cast<void *>(p)) == hipSuccess &&
+                a - reinterpret_cast<uintptr_t>(base) < size) {
+                last_lo_ = reinterpret_cast<uintptr_t>(base);
+                last_size_ = size;
+                known_[last_lo_] = size;
+            } else {
+                (void)hipGetLastError();
+            }
+        }
+        return true;
+    }
+
+  private:
+    std::map<uintptr_t, size_t> known_;  // allocation start -> size
+    uintptr_t last_lo_ = 0;
+    size_t last_size_ = 0;
+};
 
 // A vector kernel's tile is 256 elements (a one-wave block of 64 lanes x 4
 // elements): 1 KiB of every 4-byte array.  Tiles that start on a 1 KiB
@@ -344,8 +392,9 @@ struct Tagged {
 // end of the earlier one, which the sweep keeps as the largest end so far.
 bool written_overlap(std::vector<Tagged> &spans)
 {
-    std::sort(spans.begin(), spans.end(),
-              [](const Tagged &a, const Tagged &b) { return a.lo < b.lo; });
+    const auto by_start = [](const Tagged &a, const Tagged &b) { return a.lo < b.lo; };
+    if (!std::is_sorted(spans.begin(), spans.end(), by_start))
+        std::sort(spans.begin(), spans.end(), by_start);
     uintptr_t max_end = 0, max_out_end = 0;
     for (const Tagged &t : spans) {
         if (t.lo < max_out_end || (t.out && t.lo < max_end))
@@ -456,46 +505,53 @@ disdp_status_t disdp_aggregate_adam_multi(const void *const *grads, int W,
     if (!grads || !param || !m || !v)
         return DISDP_ERR_INVALID_ARG;
     const int gb = grad_bytes(gdtype);
-    std::vector<Tagged> spans;
-    spans.reserve(static_cast<size_t>(T) * (W + 4));
     for (int j = 0; j < T; ++j) {
         if (n[j] == 0)
             continue;
-        for (int w = 0; w < W; ++w) {
-            const void *g = grads[static_cast<int64_t>(j) * W + w];
-            if (!g)
+        for (int w = 0; w < W; ++w)
+            if (!grads[static_cast<int64_t>(j) * W + w])
                 return DISDP_ERR_INVALID_ARG;
-            const Span sp = span_of(g, n[j], gb);
-            spans.push_back({sp.lo, sp.hi, false});
-        }
         if (!param[j] || !m[j] || !v[j])
             return DISDP_ERR_INVALID_ARG;
-        const void *outs[] = {param[j], m[j], v[j]};
-        for (const void *o : outs) {
-            const Span sp = span_of(o, n[j], 4);
-            spans.push_back({sp.lo, sp.hi, true});
-        }
-        if (param_bf16_out && param_bf16_out[j]) {
-            const Span sp = span_of(param_bf16_out[j], n[j], 2);
-            spans.push_back({sp.lo, sp.hi, true});
-        }
     }
+    // Array by array: when every array holds its tensors in address order
+    // (sub-ranges of flat shard arrays) the list arrives sorted.
+    std::vector<Tagged> spans;
+    spans.reserve(static_cast<size_t>(T) * (W + 4) + 1);
+    auto add = [&](auto arr, int64_t stride, int esz, bool out) {
+        for (int j = 0; j < T; ++j) {
+            const void *p = arr[static_cast<int64_t>(j) * stride];
+            if (n[j] > 0 && p) {
+                const Span sp = span_of(p, n[j], esz);
+                spans.push_back({sp.lo, sp.hi, out});
+            }
+        }
+    };
+    for (int w = 0; w < W; ++w)
+        add(grads + w, W, gb, false);
+    add(param, 1, 4, true);
+    add(m, 1, 4, true);
+    add(v, 1, 4, true);
+    if (param_bf16_out)
+        add(param_bf16_out, 1, 2, true);
     if (scalars) {
         const Span sp = span_of(scalars, 1, sizeof(disdp_step_scalars_t));
         spans.push_back({sp.lo, sp.hi, false});
     }
     if (written_overlap(spans))
         return DISDP_ERR_ALIAS;
-    if (scalars && !gpu_addressable(scalars))
+    AddressableSet addressable;
+    if (scalars && !addressable.check(scalars))
         return DISDP_ERR_INVALID_ARG;
     for (int j = 0; j < T; ++j) {
         if (n[j] == 0)
             continue;
         for (int w = 0; w < W; ++w)
-            if (!gpu_addressable(grads[static_cast<int64_t>(j) * W + w]))
+            if (!addressable.check(grads[static_cast<int64_t>(j) * W + w]))
                 return DISDP_ERR_INVALID_ARG;
-        if (!gpu_addressable(param[j]) || !gpu_addressable(m[j]) || !gpu_addressable(v[j]) ||
-            (param_bf16_out && param_bf16_out[j] && !gpu_addressable(param_bf16_out[j])))
+        if (!addressable.check(param[j]) || !addressable.check(m[j]) ||
+            !addressable.check(v[j]) ||
+            (param_bf16_out && param_bf16_out[j] && !addressable.check(param_bf16_out[j])))
             return DISDP_ERR_INVALID_ARG;
     }
 

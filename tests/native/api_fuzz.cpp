@@ -24,6 +24,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <set>
 #include <vector>
 
 #include "disdp.h"
@@ -67,14 +68,33 @@ hipError_t launch_quantize(const QuantizeArgs &q, bool vector_path, hipStream_t)
 }
 }  // namespace disdp
 
+// Device memory is modelled as 64 GiB allocations aligned to their size,
+// except one 1 TiB region that the GPU cannot address.
+constexpr uintptr_t kAllocBytes = uintptr_t(1) << 36;
+constexpr uintptr_t kBadLo = uintptr_t(1) << 50, kBadHi = kBadLo + (uintptr_t(1) << 40);
+bool unaddressable(const void *p)
+{
+    const uintptr_t a = reinterpret_cast<uintptr_t>(p);
+    return !g_addressable || (a >= kBadLo && a < kBadHi);
+}
+
 extern "C" hipError_t hipPointerGetAttributes(hipPointerAttribute_t *at, const void *p)
 {
     ++g_queries;
     std::memset(at, 0, sizeof *at);
-    if (!g_addressable)
+    if (unaddressable(p))
         return hipErrorInvalidValue;
     at->type = hipMemoryTypeDevice;
     at->devicePointer = const_cast<void *>(p);
+    return hipSuccess;
+}
+
+extern "C" hipError_t hipMemGetAddressRange(hipDeviceptr_t *base, size_t *size, hipDeviceptr_t p)
+{
+    if (unaddressable(p))
+        return hipErrorInvalidValue;
+    *base = reinterpret_cast<hipDeviceptr_t>(reinterpret_cast<uintptr_t>(p) & ~(kAllocBytes - 1));
+    *size = kAllocBytes;
     return hipSuccess;
 }
 
@@ -552,6 +572,23 @@ void fuzz_multi(int iters)
         g_singles.clear();
         g_single_vec.clear();
         g_multis.clear();
+        // one runtime query per allocation touched, however many arrays it holds
+        std::set<uintptr_t> allocs;
+        for (int j = 0; j < T; ++j) {
+            if (n[j] == 0)
+                continue;
+            for (int w = 0; w < W; ++w)
+                allocs.insert(reinterpret_cast<uintptr_t>(g[static_cast<size_t>(j) * W + w]) /
+                              kAllocBytes);
+            for (const void *q : {static_cast<const void *>(p[j]), static_cast<const void *>(m[j]),
+                                  static_cast<const void *>(v[j]),
+                                  static_cast<const void *>(copies ? p16[j] : nullptr)})
+                if (q)
+                    allocs.insert(reinterpret_cast<uintptr_t>(q) / kAllocBytes);
+        }
+        if (sc && !allocs.empty())
+            allocs.insert(reinterpret_cast<uintptr_t>(sc) / kAllocBytes);
+        const int queries = g_queries;
         const disdp_status_t st = disdp_aggregate_adam_multi(
             g.data(), W, static_cast<disdp_dtype_t>(gdt), T, n.data(),
             static_cast<disdp_agg_mode_t>(mode), 24, p.data(), m.data(), v.data(),
@@ -559,6 +596,13 @@ void fuzz_multi(int iters)
         CHECK(st == DISDP_OK, "multi: status %d (T=%d W=%d)", st, T, W);
         if (st != DISDP_OK)
             continue;
+        // plus the single-tensor path's own checks of every array it is given
+        int single_queries = 0;
+        for (const disdp::LaunchArgs &a : g_singles)
+            single_queries += W + 3 + (a.p16 ? 1 : 0) + (a.s_dev ? 1 : 0);
+        CHECK(g_queries - queries <= static_cast<int>(allocs.size()) + single_queries,
+              "multi: %d pointer queries for %zu allocations and %zu single launches",
+              g_queries - queries, allocs.size(), g_singles.size());
         const int per = W + 4;
         const int cap = std::min(disdp::kMultiMaxTensors, disdp::kMultiMaxPtrs / per);
         std::vector<int> seen(T, 0);
@@ -620,7 +664,7 @@ void fuzz_multi(int iters)
                 j0 = k;
         if (j0 < 0)
             continue;
-        const int kind = static_cast<int>(below(6));
+        const int kind = static_cast<int>(below(7));
         disdp_status_t want = DISDP_OK;
         std::vector<float *> p2 = p, m2 = m;
         std::vector<const void *> g2 = g;
@@ -656,8 +700,18 @@ void fuzz_multi(int iters)
             want = DISDP_ERR_INVALID_ARG;
         } else if (kind == 4) {  // step constants: both sources, none, or misaligned
             want = DISDP_ERR_INVALID_ARG;
-        } else {                 // device step constants inside an output
+        } else if (kind == 5) {  // device step constants inside an output
             want = DISDP_ERR_ALIAS;
+        } else {                 // one array of tensor j0 in memory the GPU cannot address
+            char *bad = reinterpret_cast<char *>(kBadLo) + 4096 * below(1 << 20);
+            const int which = static_cast<int>(below(W + 2));
+            if (which < W)
+                g2[static_cast<size_t>(j0) * W + which] = bad;
+            else if (which == W)
+                p2[j0] = reinterpret_cast<float *>(bad);
+            else
+                m2[j0] = reinterpret_cast<float *>(bad);
+            want = DISDP_ERR_INVALID_ARG;
         }
         const disdp_adamw_hparams_t *hp2 = dev ? nullptr : &hp;
         const disdp_step_scalars_t *sc2 = sc;
