@@ -572,7 +572,6 @@ def run_layers(args):
     refreshes the step's constants; (d) one disdp_aggregate_adam_multi call
     (a batch of tensors per launch); (e) that call with the constants in
     device memory, captured once as a HIP graph with its copy node."""
-    import ctypes
     import numpy as np
     import torch
     import paper_2409_00918_amd as dd
@@ -619,12 +618,9 @@ def run_layers(args):
     def replay(t):
         graph.replay()
 
-    # the multi-tensor call with its host arrays built once (the library
-    # still checks every pointer on every call)
-    mgrads = dd.host_array([g.data_ptr() for ta in tensor_args for g in ta[0]])
-    mns = dd.host_array([ta[1].numel() for ta in tensor_args], ctypes.c_int64)
-    mp, mm, mv, m16 = (dd.host_array([ta[i].data_ptr() for ta in tensor_args])
-                       for i in (1, 2, 3, 4))
+    # the multi-tensor call with the tensors checked and packed once (the
+    # library still checks every allocation on every call)
+    mstep = dd.MultiTensorStep(tensor_args)
 
     mgraph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(mgraph, stream=side):
@@ -636,12 +632,7 @@ def run_layers(args):
         mgraph.replay()
 
     def multi(t):
-        st = dd.raw_aggregate_adam_multi(
-            mgrads, wl.W, dd.DT_F32, len(tensor_args), mns, dd.AGG_FP32, 0, mp, mm, mv, m16,
-            dd.AdamWHParams(kw["lr"], kw["beta1"], kw["beta2"], kw["eps"], kw["weight_decay"],
-                            t, 1.0), s.cuda_stream)
-        if st != dd.OK:
-            raise dd.DisdpError(st, "disdp_aggregate_adam_multi")
+        mstep(step=t, **kw)
 
     def prepare(t, mode):
         torch.cuda.synchronize()            # a previous replay has read `host`

@@ -22,6 +22,8 @@ call raises.
                        device memory (one HIP graph for every step)
 ``aggregate_adam_multi`` -- the fused call over many tensors in separate
                        buffers (a batch of tensors per launch)
+``MultiTensorStep`` -- the same over a fixed list of tensors, checked and
+                       packed once, one step per call
 """
 from __future__ import annotations
 
@@ -279,8 +281,12 @@ def _launch(fn, tensors, stream, *args):
     """Call `fn(*args, hip_stream)` with the tensors' GPU current: the
     library launches on the current device.  The stream is the one given,
     else torch's current stream of that device."""
+    return _launch_on(_device_index(tensors), stream, fn, *args)
+
+
+def _launch_on(idx, stream, fn, *args):
+    """_launch for tensors known to live on GPU `idx` (-1: none does)."""
     torch = _torch()
-    idx = _device_index(tensors)
     cur = torch.cuda.current_device()
     if idx < 0:
         idx = cur
@@ -399,43 +405,79 @@ def aggregate_adam_dev(grads, param, m, v, param_bf16_out=None, *, scalars,
     _check(st, "disdp_aggregate_adam_dev")
 
 
+class MultiTensorStep:
+    """disdp_aggregate_adam_multi over a fixed list of tensors, for a caller
+    that steps the same tensors again and again: the tensors are checked
+    and their pointers packed into host arrays once, and each call takes
+    one step.  `tensors`: a sequence of (grads, param, m, v, param_bf16_out)
+    with grads a list of W contributions of that tensor's length and
+    param_bf16_out possibly None.  The object keeps the tensors alive."""
+
+    def __init__(self, tensors, *, mode="fp32", frac_bits: int = 0):
+        torch = _torch()
+        self._tensors = list(tensors)
+        self._mode = _mode(mode)
+        self._frac_bits = frac_bits
+        self.T = len(self._tensors)
+        if not self._tensors:
+            return
+        W = len(self._tensors[0][0])
+        gdt = _grad_dtype(self._tensors[0][0][0])
+        allowed = {DT_F32: (torch.float32,), DT_I32: (torch.int32,)}.get(
+            gdt, (torch.bfloat16, torch.int16, torch.uint16))
+        f32 = (torch.float32,)
+        p16t = (torch.bfloat16, torch.int16, torch.uint16)
+        gp, ns, ps, ms_, vs, cs, every = [], [], [], [], [], [], []
+        for j, (grads, p, m, v, c) in enumerate(self._tensors):
+            if len(grads) != W:
+                raise ValueError(f"tensor {j} has {len(grads)} contributions, expected {W}")
+            n = p.numel()
+            gp += [_dev_ptr(g, f"tensors[{j}] grads[{w}]", n, allowed)
+                   for w, g in enumerate(grads)]
+            ns.append(n)
+            ps.append(_dev_ptr(p, f"tensors[{j}] param", n, f32))
+            ms_.append(_dev_ptr(m, f"tensors[{j}] m", n, f32))
+            vs.append(_dev_ptr(v, f"tensors[{j}] v", n, f32))
+            cs.append(_dev_ptr(c, f"tensors[{j}] param_bf16_out", n, p16t))
+            every += list(grads) + [p, m, v, c]
+        self.W = W
+        self._gdt = gdt
+        self._device = _device_index(every)
+        self._arrays = (host_array(gp), host_array(ns, ctypes.c_int64), host_array(ps),
+                        host_array(ms_), host_array(vs), host_array(cs) if any(cs) else None)
+
+    def __call__(self, *, lr=None, beta1=None, beta2=None, eps=None, weight_decay=None,
+                 step=None, grad_scale=1.0, scalars=None, stream=None) -> None:
+        """One step of every tensor: the hyperparameters, or `scalars` (as
+        for aggregate_adam_dev) instead."""
+        if not self.T:
+            return
+        hp = None if scalars is not None else \
+            _hparams(lr, beta1, beta2, eps, weight_decay, step, grad_scale)
+        sc = _dev_ptr(scalars, "scalars", ctypes.sizeof(StepScalars) // 4, (_torch().float32,))
+        idx = self._device
+        if scalars is not None:
+            d = _device_index([scalars])
+            if idx >= 0 and d >= 0 and d != idx:
+                raise ValueError(f"scalars on cuda:{d}, tensors on cuda:{idx}")
+            idx = d if idx < 0 else idx
+        gp, ns, ps, ms_, vs, cs = self._arrays
+        st = _launch_on(idx, stream, lambda *a: raw_aggregate_adam_multi(
+            *a[:-1], stream=a[-1], scalars=sc),
+            gp, self.W, self._gdt, self.T, ns, self._mode, self._frac_bits, ps, ms_, vs, cs, hp)
+        _check(st, "disdp_aggregate_adam_multi")
+
+
 def aggregate_adam_multi(tensors, *, lr=None, beta1=None, beta2=None, eps=None,
                          weight_decay=None, step=None, grad_scale=1.0, scalars=None,
                          mode="fp32", frac_bits: int = 0, stream=None) -> None:
     """aggregate_adam over many tensors at once (a batch of tensors per
-    launch).  `tensors`: a sequence of (grads, param, m, v, param_bf16_out)
-    with grads a list of W contributions of that tensor's length and
-    param_bf16_out possibly None.  Every tensor takes the same step: the
-    hyperparameters, or `scalars` (as for aggregate_adam_dev) instead."""
-    torch = _torch()
-    tensors = list(tensors)
-    if not tensors:
-        return
-    W = len(tensors[0][0])
-    gdt = _grad_dtype(tensors[0][0][0])
-    allowed = {DT_F32: (torch.float32,), DT_I32: (torch.int32,)}.get(
-        gdt, (torch.bfloat16, torch.int16, torch.uint16))
-    f32 = (torch.float32,)
-    p16t = (torch.bfloat16, torch.int16, torch.uint16)
-    gp, ns, ps, ms_, vs, cs, every = [], [], [], [], [], [], []
-    for j, (grads, p, m, v, c) in enumerate(tensors):
-        if len(grads) != W:
-            raise ValueError(f"tensor {j} has {len(grads)} contributions, expected {W}")
-        n = p.numel()
-        gp += [_dev_ptr(g, f"tensors[{j}] grads[{w}]", n, allowed) for w, g in enumerate(grads)]
-        ns.append(n)
-        ps.append(_dev_ptr(p, f"tensors[{j}] param", n, f32))
-        ms_.append(_dev_ptr(m, f"tensors[{j}] m", n, f32))
-        vs.append(_dev_ptr(v, f"tensors[{j}] v", n, f32))
-        cs.append(_dev_ptr(c, f"tensors[{j}] param_bf16_out", n, p16t))
-        every += list(grads) + [p, m, v, c]
-    hp = None if scalars is not None else \
-        _hparams(lr, beta1, beta2, eps, weight_decay, step, grad_scale)
-    sc = _dev_ptr(scalars, "scalars", ctypes.sizeof(StepScalars) // 4, f32)
-    st = _launch(lambda *a: raw_aggregate_adam_multi(*a[:-1], stream=a[-1], scalars=sc),
-                 every + [scalars], stream, gp, W, gdt, len(tensors), ns,
-                 _mode(mode), frac_bits, ps, ms_, vs, cs if any(cs) else None, hp)
-    _check(st, "disdp_aggregate_adam_multi")
+    launch); the tensors as for MultiTensorStep, which a caller stepping
+    the same tensors repeatedly should keep instead.  Every tensor takes
+    the same step: the hyperparameters, or `scalars` instead."""
+    MultiTensorStep(tensors, mode=mode, frac_bits=frac_bits)(
+        lr=lr, beta1=beta1, beta2=beta2, eps=eps, weight_decay=weight_decay, step=step,
+        grad_scale=grad_scale, scalars=scalars, stream=stream)
 
 
 def quantize(grad, out, *, frac_bits: int, stream=None) -> None:

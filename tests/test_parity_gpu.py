@@ -1188,6 +1188,49 @@ def test_multi_tensor_call_equals_one_call_per_tensor(W, T):
                 assert t_.equal(u, w), _label(j=j, n=sizes[j], copies=copies)
 
 
+@pytest.mark.parametrize("gdtype,mode", [("f32", "fp32"), ("bf16", "fixed")])
+def test_multi_tensor_step_object_over_steps(gdtype, mode):
+    """MultiTensorStep (tensors checked and packed once) stepped four times
+    with fresh contributions written into the same buffers: every tensor
+    against the oracle's own trajectory each step, and bit-equal to one
+    aggregate_adam_multi call per step on copies of the state."""
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    rng = np.random.default_rng(3100)
+    W = 5
+    a, host = _multi_tensors(rng, 30, W, gdtype, unrelated=True, seed=3200)
+    b = [(dg, dp.clone(), dm.clone(), dv.clone(), d16.clone()) for dg, dp, dm, dv, d16 in a]
+    step = dd.MultiTensorStep(a, mode=mode, frac_bits=24)
+    assert step.T == 30 and step.W == W
+    state = [(p.copy(), m.copy(), v.copy()) for _, p, m, v in host]
+    kw = dict(lr=HP["lr"], beta1=HP["beta1"], beta2=HP["beta2"], eps=HP["eps"],
+              weight_decay=HP["wd"])
+    for t in range(1, 5):
+        fresh = []
+        for j, (dg, *_rest) in enumerate(a):
+            n = dg[0].numel()
+            gs = synth.host_grads(3300 + 10 * t + j, t, W, n, 1e-4, gdtype=gdtype)
+            for d, g in zip(dg, gs):
+                d.copy_(t_.from_numpy(np.ascontiguousarray(
+                    g.view(np.int16) if g.dtype == np.uint16 else g)))
+            fresh.append(gs)
+        step(step=t, **kw)
+        dd.aggregate_adam_multi(b, step=t, mode=mode, frac_bits=24, **kw)
+        t_.cuda.synchronize()
+        for j, ((dg, dp, dm, dv, d16), gs) in enumerate(zip(a, fresh)):
+            p, m, v = state[j]
+            want = oracle.fused(gs, p, m, v, mode=oracle.AGG_FIXED if mode == "fixed"
+                                else oracle.AGG_FP32, frac_bits=24, t=t, **HP)
+            assert_parity({"p": to_host(dp), "m": to_host(dm), "v": to_host(dv),
+                           "p16": to_host(d16)}, want, _label(t=t, j=j, n=p.size))
+            state[j] = (want["p"], want["m"], want["v"])
+            for u, w in zip((dp, dm, dv, d16), b[j][1:]):
+                assert t_.equal(u, w), _label(t=t, j=j)
+    with pytest.raises(TypeError):
+        step(step=5)                       # neither hyperparameters nor scalars
+    dd.MultiTensorStep([])(step=1, **kw)   # no tensors: nothing to do
+
+
 def test_multi_tensor_call_captured_in_a_hip_graph():
     """The multi-tensor call enqueues kernel launches only: captured once,
     replayed three times with eager work between, it equals the same call
