@@ -645,7 +645,7 @@ def run_layers(args):
     res = {k: [] for k in modes}
     host_ms = {k: [] for k in modes}
     t = 0
-    for rnd in range(4 + 1):
+    for rnd in range(4 + 1):            # pass 0 warms up, passes 1-4 are timed
         for name, fn in modes.items():
             for _ in range(args.steps if rnd else 1):
                 t += 1
@@ -658,7 +658,7 @@ def run_layers(args):
                 h1 = time.perf_counter()
                 b.record(s)
                 torch.cuda.synchronize()
-                if rnd:                      # round 0 warms every mode up
+                if rnd:                      # the first pass warms every mode up
                     res[name].append(a.elapsed_time(b))
                     host_ms[name].append((h1 - h0) * 1e3)
     out = {}
