@@ -635,14 +635,19 @@ def contiguous_bytes(nbytes: int, device="cuda"):
     return t
 
 
+CONTIGUOUS_MIN_BYTES = 1 << 30   # smallest shard slab given a contiguous block
+
+
 class Shard:
     """A shard's arrays as torch views of one device allocation (`slab`):
     grads (W tensors), param, m, v, and when requested param_bf16 (int16
     bits), agg_f32, agg_i32.  Contents are uninitialised.
 
-    With `contiguous` (the default) the slab is one physically contiguous
-    block of device memory (`self.contiguous` says whether the runtime had
-    one; otherwise torch's caching allocator provides the slab).  On MI355X
+    With `contiguous` (the default) a slab of at least CONTIGUOUS_MIN_BYTES
+    is one physically contiguous block of device memory (`self.contiguous`
+    says whether the runtime had one; otherwise, and for smaller slabs,
+    torch's caching allocator provides it: a pooled block is kept for the
+    life of the process, which only large shards are worth).  On MI355X
     the fused kernel streams such a slab at 6.50-6.56 TB/s in every fresh
     process tried, against 6.34-6.55 for ordinary allocations, whose
     physical pages vary from process to process."""
@@ -652,7 +657,8 @@ class Shard:
         torch = _torch()
         offs, total = shard_layout(n, W, gdtype, bf16_copy=bf16_copy, agg_f32=agg_f32,
                                    agg_i32=agg_i32)
-        slab = contiguous_bytes(total, device) if contiguous and total > 0 else None
+        slab = contiguous_bytes(total, device) \
+            if contiguous and total >= CONTIGUOUS_MIN_BYTES else None
         self.contiguous = slab is not None
         self.slab = slab if slab is not None else \
             torch.empty(total, dtype=torch.uint8, device=device)

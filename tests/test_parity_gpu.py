@@ -1042,6 +1042,9 @@ def test_contiguous_shard_slab_lifetime():
     del a, b
     gc.collect()
     assert dd.contiguous_pool()[1] == leased0
+    # a small shard is not worth a block kept for the life of the process
+    small = dd.allocate_shard(100_000, W, "f32")
+    assert not small.contiguous and dd.contiguous_pool()[1] == leased0
 
 
 def test_pooled_block_waits_for_work_queued_on_it():
