@@ -169,18 +169,18 @@ __device__ __forceinline__ uint32_t to_bf16(float x)
 }
 
 // Contribution -> int32 at scale 2^k: exact scaling, rint (ties to even),
-// saturation, NaN -> 0.  Written without branches (selects only): the
-// rounded value is clamped in float to [-2^31, 2^31 - 128] -- no float lies
-// strictly between 2^31 - 128 and 2^31 -- so the conversion is always in
-// range and exact; values >= 2^31 then select INT32_MAX and NaN selects 0.
+// saturation, NaN -> 0 (the integer switch format, Section III-B), in three
+// instructions and no branches.
 __device__ __forceinline__ int32_t quantize(float x, float scale)
 {
-    const float y = x * scale;
-    const float r = __builtin_rintf(y);
-    const float c = __builtin_fminf(__builtin_fmaxf(r, -2147483648.0f), 2147483520.0f);
-    int32_t q = static_cast<int32_t>(c);
-    q = r >= 2147483648.0f ? INT32_MAX : q;
-    return y != y ? 0 : q;
+    const float r = __builtin_rintf(x * scale);
+    // The hardware conversion already has the format's saturation: a float
+    // at or above 2^31 (+inf included) gives INT32_MAX, one below -2^31
+    // (-inf included) INT32_MIN, NaN 0, anything else its (integral) value.
+    // A C++ cast leaves those cases undefined, hence the instruction itself.
+    int32_t q;
+    asm("v_cvt_i32_f32 %0, %1" : "=v"(q) : "v"(r));
+    return q;
 }
 
 __device__ __forceinline__ int32_t saturate32(int64_t s)
@@ -657,20 +657,22 @@ __global__ DISDP_QUANT_LAUNCH_BOUNDS void quantize_element_kernel(QuantizeArgs q
 constexpr int kU = DISDP_UNROLL;
 
 // Resident waves per CU for a fixed-point kernel converting float
-// contributions, whose lanes spend ~4x more instructions per element than
-// in fp32 mode and so hold loads in flight for a smaller share of the time.
-// The best cap falls with the bytes a lane keeps in flight and rises with
-// the conversions per byte (bf16 contributions have twice as many).
-// Interleaved A/B of the fused call at n = 4e8 over caps of 8-16 (TB/s at
-// the chosen cap vs the next best): fp32 W = 1, 2 (64, 80 B) 14; W = 4
-// (112 B) 12; W = 8 (176 B) 10, with 8 within 0.3%; W = 12, 16 (240,
-// 304 B) 8; bf16 W = 8, 16 14.  Int32 contributions need no conversion and
-// take the fp32-mode caps.
+// contributions, by the bytes of loads a lane keeps in flight, as in fp32
+// mode; a lane converting bf16 contributions (twice the conversions per
+// byte) holds its loads for a smaller share of the time and wants more
+// waves.  Interleaved A/B of the fused call at n = 4e8 over caps of 6-14
+// (TB/s at the chosen cap, the next best in brackets): fp32 W = 1, 2
+// (64, 80 B) 14: 6.48, 6.49 (12: 6.28, 6.41); W = 4 (112 B) 12: 6.61;
+// W = 8 (176 B) 8: 6.59 (10: 6.49); W = 12, 24 (240, 432 B) 6: 6.44, 6.04
+// (8: 6.24, 6.01); bf16 W = 4 (80 B) 14: 6.43 (12: 6.28); W = 8 (112 B)
+// 12: 6.38 (14: 6.34); W = 16, 32 (176, 304 B) 10: 6.19, 6.00 (8: 6.16,
+// 5.93).  Int32 contributions need no conversion and take the fp32-mode
+// caps.
 constexpr int fixed_mode_waves(int lane_bytes, bool bf16)
 {
     if (DISDP_WAVES_PER_CU_FIXED > 0)
         return DISDP_WAVES_PER_CU_FIXED;
-    return bf16 || lane_bytes <= 80 ? 14 : lane_bytes <= 112 ? 12 : lane_bytes <= 176 ? 10 : 8;
+    return lane_bytes <= 80 ? 14 : lane_bytes <= 112 ? 12 : bf16 ? 10 : lane_bytes <= 176 ? 8 : 6;
 }
 
 // Resident waves per CU in fp32 mode (and for int32 contributions), by the
@@ -688,9 +690,13 @@ constexpr int fp32_mode_waves(int lane_bytes)
 
 // The same for the run-time worker-count kernel, from the actual W: whole
 // chunks keep 128 B per lane in flight (8 waves suffice), a remainder adds
-// round trips with fewer bytes (10, 12 in fixed mode), and W below one
-// chunk is all such pieces (14).  Measured for fp32 W = 9, 24, 64 and bf16
-// W = 13, 32, 64 in both modes.
+// round trips with fewer bytes (10), and W below one chunk is all such
+// pieces (14).  Measured for fp32 W = 9, 24, 64 and bf16 W = 13, 32, 64.
+// Converting bf16 in fixed mode wants two more waves.  Fixed mode at
+// n = 4e8 over caps of 6-14 (TB/s at the chosen cap, the next best in
+// brackets): fp32 W = 9, 13, 20 10: 6.55, 6.47, 6.33 (12: 6.51; 8: 6.44,
+// 6.32); W = 24 8: 6.21 (6: 6.25); bf16 W = 17, 40 12: 6.35, 6.17 (14:
+// 6.24, 6.06); W = 32 10: 6.05 (12: 5.97).
 int runtime_w_waves(int W, int gt, int mode)
 {
     const bool bf16 = gt == kGradBF16;
@@ -698,7 +704,7 @@ int runtime_w_waves(int W, int gt, int mode)
     if (mode == kAggFixed && gt != kGradI32) {
         if (DISDP_WAVES_PER_CU_FIXED > 0)
             return DISDP_WAVES_PER_CU_FIXED;
-        return bf16 ? 14 : W % chunk ? 12 : 8;
+        return (W % chunk ? 10 : 8) + (bf16 ? 2 : 0);
     }
     if (DISDP_WAVES_PER_CU != 0)
         return DISDP_WAVES_PER_CU > 0 ? DISDP_WAVES_PER_CU : 0;
