@@ -497,3 +497,27 @@ def test_multi_takes_exactly_one_source_of_step_constants():
     # a valid combination gets as far as the (fake, unmapped) addresses
     assert call(None, base) == dd.ERR_INVALID_ARG
     assert call(hp(), 0) == dd.ERR_INVALID_ARG
+
+
+def test_multi_accepts_host_arrays_built_once():
+    """host_array packs pointer and size lists once; the raw call takes the
+    packed arrays as it takes lists, with the same checks."""
+    T, W = 3, 4
+    base = lambda j, i: 0x20_0000_0000 + (j * 16 + i) * 0x1_0000_0000
+    grads = [base(j, w) for j in range(T) for w in range(W)]
+    params = [base(0, 12), base(2, 2) + 64, base(2, 12)]       # tensor 1 inside a contribution
+    ms = [base(j, 13) for j in range(T)]
+    vs = [base(j, 14) for j in range(T)]
+    assert dd.host_array(None) is None
+    g = dd.host_array(grads)
+    assert dd.host_array(g) is g and [x or 0 for x in g] == grads
+    ns = dd.host_array([N] * T, ctypes.c_int64)
+    assert list(ns) == [N] * T
+    packed = (g, W, dd.DT_F32, T, ns, dd.AGG_FP32, 0, dd.host_array(params), dd.host_array(ms),
+              dd.host_array(vs), None, hp(), 0)
+    listed = (grads, W, dd.DT_F32, T, [N] * T, dd.AGG_FP32, 0, params, ms, vs, None, hp(), 0)
+    assert dd.raw_aggregate_adam_multi(*packed) == dd.ERR_ALIAS
+    assert dd.raw_aggregate_adam_multi(*listed) == dd.ERR_ALIAS
+    # NULL entries survive packing (0 -> NULL)
+    z = dd.host_array([0, base(0, 0)])
+    assert z[0] is None and z[1] == base(0, 0)
