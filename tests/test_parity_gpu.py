@@ -1234,6 +1234,54 @@ def test_multi_tensor_step_object_over_steps(gdtype, mode):
     dd.MultiTensorStep([])(step=1, **kw)   # no tensors: nothing to do
 
 
+def test_multi_tensor_call_with_pinned_host_state_and_on_a_cu_masked_stream():
+    """The many-tensor call with every tensor's p, m, v and bf16 copy in
+    pinned host memory (contributions in HBM): each tensor against the
+    oracle; and on CU-masked streams (a raised occupancy cap), bit-equal to
+    the default stream."""
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    W, sizes = 4, [5, 4099, 0, 250_001, 257, 64]
+    kw = dict(lr=HP["lr"], beta1=HP["beta1"], beta2=HP["beta2"], eps=HP["eps"],
+              weight_decay=HP["wd"], step=2)
+    for mode in ("fp32", "fixed"):
+        tensors, want = [], []
+        for j, n in enumerate(sizes):
+            gs = synth.host_grads(4000 + j, 1, W, n, 1e-4, outlier_frac=0.01, outlier_scale=100.0)
+            p, m, v = synth.host_state(4000 + j, n, mv_sigma=1e-4)
+            host = _pinned if n else to_dev    # an empty tensor has no pinned storage
+            tensors.append(([to_dev(g) for g in gs], host(p), host(m), host(v),
+                            host(np.zeros(n, np.uint16))))
+            want.append(oracle.fused(gs, p, m, v, t=2, mode=oracle.AGG_FIXED if mode == "fixed"
+                                     else oracle.AGG_FP32, frac_bits=24, **HP))
+        dd.aggregate_adam_multi(tensors, mode=mode, frac_bits=24, **kw)
+        t_.cuda.synchronize()
+        for j, ((_, hp_, hm, hv, h16), w) in enumerate(zip(tensors, want)):
+            got = {"p": to_host(hp_), "m": to_host(hm), "v": to_host(hv), "p16": to_host(h16)}
+            assert_parity(got, w, _label(host_state=mode, j=j, n=sizes[j]))
+    rng = np.random.default_rng(4100)
+    a, _ = _multi_tensors(rng, 30, 8, "f32", unrelated=True, seed=4200)
+    state0 = [[x.clone() for x in (dp, dm, dv, d16)] for _, dp, dm, dv, d16 in a]
+    dd.aggregate_adam_multi(a, **kw)
+    t_.cuda.synchronize()
+    ref = [[x.clone() for x in (dp, dm, dv, d16)] for _, dp, dm, dv, d16 in a]
+    for n_cus in (32, 200):
+        for (_, dp, dm, dv, d16), st in zip(a, state0):
+            for dst, src in zip((dp, dm, dv, d16), st):
+                dst.copy_(src)
+        t_.cuda.synchronize()
+        s, h, hip = _cu_masked_stream(n_cus)
+        try:
+            dd.aggregate_adam_multi(a, stream=s, **kw)
+            s.synchronize()
+            for j, ((_, dp, dm, dv, d16), r) in enumerate(zip(a, ref)):
+                for u, w in zip((dp, dm, dv, d16), r):
+                    assert t_.equal(u, w), _label(cus=n_cus, j=j)
+        finally:
+            t_.cuda.synchronize()
+            hip.hipStreamDestroy(h)
+
+
 def test_multi_tensor_call_captured_in_a_hip_graph():
     """The multi-tensor call enqueues kernel launches only: captured once,
     replayed three times with eager work between, it equals the same call
