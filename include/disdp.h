@@ -254,9 +254,12 @@ disdp_status_t disdp_aggregate_adam_dev(const void *const *grads, int W,
  * skipped (their pointers may be NULL).  Checks as for disdp_aggregate_adam,
  * over all tensors together: no output of any tensor may overlap any other
  * buffer of any tensor (DISDP_ERR_ALIAS; contributions may overlap one
- * another).  Alignment as for the other calls, per tensor.  The checks use
- * host memory proportional to T * (W + 4); a launch failure after earlier
- * batches were enqueued returns DISDP_ERR_HIP. */
+ * another).  Alignment as for the other calls, per tensor.  The runtime is
+ * asked about each device allocation the pointers fall in once per call, so
+ * tensors carved out of a few large allocations are checked in a few
+ * queries.  The checks use host memory proportional to T * (W + 4); a
+ * launch failure after earlier batches were enqueued returns
+ * DISDP_ERR_HIP. */
 disdp_status_t disdp_aggregate_adam_multi(const void *const *grads, int W,
                                           disdp_dtype_t gdtype, int T, const int64_t *n,
                                           disdp_agg_mode_t mode, int frac_bits,
