@@ -87,6 +87,31 @@
  *             operation, no fused multiply-add, denormals kept; results are
  *             a deterministic function of the inputs (no atomics, no
  *             dependence on grid size).
+ * Sharing     The kernels are memory-bound and by default launch one-wave
+ *             blocks, the fastest shape when they have the GPU to
+ *             themselves.  On a GPU whose compute kernels run at the same
+ *             time on other streams, that shape refills every slot a
+ *             retiring block frees: measured next to a bf16 GEMM loop on the
+ *             7B/8 shard, the GEMM slowed about 10x and the fused call 1.1x.
+ *             Two knobs trade this, neither changing any result:
+ *               - DISDP_LAUNCH_SHAPE=shared in the environment (read on every
+ *                 call) selects four-wave blocks with one occupancy cap per
+ *                 mode, which share an unmasked chip more evenly (about 2x
+ *                 each) at a few percent below the default rate alone;
+ *               - a CU-masked stream (hipExtStreamCreateWithCUMask) confines
+ *                 the kernels to its CUs; the library reads the mask and
+ *                 raises its per-CU occupancy cap to match.
+ *             The many-tensor call and disdp_quantize always launch
+ *             one-wave blocks.
+ * Known issue (memory from hipExtMallocWithFlags with
+ *             hipDeviceMallocContiguous; not allocated by this library):
+ *             on MI355X, after such a block was released with hipFree and
+ *             the same address range was handed out again by another
+ *             allocator, kernels read stale or zero values from memory that
+ *             had just been written by a synchronised copy.  The cause was
+ *             not found.  Callers that allocate shard memory that way should
+ *             keep those blocks for the life of the process (the Python
+ *             binding pools them) rather than freeing them.
  */
 #ifndef DISDP_H
 #define DISDP_H

@@ -106,8 +106,12 @@ bool gpu_addressable(const void *p, bool *device_memory = nullptr)
     if (device_memory)
         *device_memory = false;
     hipPointerAttribute_t at;
+    const hipError_t pending = hipPeekAtLastError();
     if (hipPointerGetAttributes(&at, p) != hipSuccess) {
-        (void)hipGetLastError();  // clear the error this query just recorded
+        // clear the error this query recorded, unless the caller already had
+        // one pending: that one must stay reported
+        if (pending == hipSuccess)
+            (void)hipGetLastError();
         return false;
     }
     switch (at.type) {
@@ -147,13 +151,14 @@ class AddressableSet {
         if (device_memory) {
             hipDeviceptr_t base = nullptr;
             size_t size = 0;
+            const hipError_t pending = hipPeekAtLastError();
             if (hipMemGetAddressRange(&base, &size, const_cast<void *>(p)) == hipSuccess &&
                 a - reinterpret_cast<uintptr_t>(base) < size) {
                 last_lo_ = reinterpret_cast<uintptr_t>(base);
                 last_size_ = size;
                 known_[last_lo_] = size;
-            } else {
-                (void)hipGetLastError();
+            } else if (pending == hipSuccess) {
+                (void)hipGetLastError();  // as in gpu_addressable
             }
         }
         return true;

@@ -11,11 +11,10 @@
 //   * one lane owns 4 consecutive elements, so every stream moves in 16-byte
 //     (fp32) or 8-byte (bf16) vector accesses and each wave instruction
 //     covers 1 KiB / 512 B of contiguous memory;
-//   * a block owns a tile of kBlock * U groups; all loads of a tile (W
-//     contributions and p, m, v for U groups) are issued before any
-//     arithmetic so each wave keeps U * (W + 3) vector loads in flight;
-//   * one tile per block over a grid that covers the shard (a persistent,
-//     occupancy-sized grid is a compile-time alternative), so every byte is
+//   * a block owns a tile of one group per lane; all loads of a lane (W
+//     contributions and p, m, v) are issued before any arithmetic, so each
+//     lane keeps W + 3 vector loads in flight;
+//   * one tile per block over a grid that covers the shard, so every byte is
 //     read once and written once;
 //   * data are touched once, so loads and stores carry the non-temporal hint;
 //   * no atomics, no cross-lane traffic: each element's reduction is one
@@ -25,102 +24,37 @@
 
 #include <atomic>
 #include <cstdint>
-#include <mutex>
+#include <cstdlib>
+#include <cstring>
 
 #include "disdp_launch.h"
 
 // One rounding per written operation: never contract a*b+c into an FMA.
 #pragma clang fp contract(off)
 
-// Launch-shape tunables (compile-time).  The defaults -- one-wave (64-lane)
-// blocks each owning one tile, one group per lane, non-temporal loads and
-// stores, tiles in natural order -- were the best or tied-best in
+// Launch shapes.  The default ("solo") shape -- one-wave (64-lane) blocks
+// each owning one tile of 64 four-element groups, non-temporal loads and
+// stores, tiles in natural order -- was the best or tied-best in
 // interleaved A/B runs on MI355X over the 7B/8, 13B/16 and 175B/64 shards;
-// the other settings were within 2% or slower (persistent grids, more
+// the alternatives measured were within 2% or slower (persistent grids, more
 // groups per lane, 128- to 1024-lane blocks, wave-contiguous groups,
 // XCD-chunked tile orders, hints on one side only).  One-wave blocks beat
 // 256-lane blocks at the same resident waves by 2-6%: a retiring wave frees
 // its slot at once instead of waiting for the slowest wave of its block.
-//   DISDP_UNROLL      groups of 4 elements per lane per tile (loads in flight)
-//   DISDP_GRID_MODE   0: persistent grid of (resident blocks per CU) x CUs x
-//                        DISDP_GRID_ROUNDS blocks, tiles grid-stride;
-//                     1: one tile per block
-//   DISDP_NT          non-temporal hints on loads (bit 0) and stores (bit 1)
-//   DISDP_BLOCK       lanes per block
-//   DISDP_WAVE_CONTIG 1: a wave's U groups are contiguous (U KiB per fp32
-//                     stream per wave); 0: strided by the block width
-//   DISDP_MIN_WAVES   launch-bounds hint: waves per SIMD to fit (0 = none)
-//   DISDP_WAVES_PER_CU  resident waves per CU for the fp32-mode vector
-//                     kernels (and int32 contributions), enforced in whole
-//                     blocks by reserving a share of the CU's LDS per block
-//                     (the kernels use no LDS): > 0 one cap for all, < 0 no
-//                     cap, 0 (default) the table of fp32_mode_waves() below.
-//                     Fewer waves than registers allow stream faster: more
-//                     outstanding requests cost DRAM efficiency.
-//   DISDP_WAVES_PER_CU_FIXED  when > 0, one cap for every fixed-point kernel
-//                     that converts float contributions; by default
-//                     (0) the cap comes from fixed_mode_waves() below.
-//                     The quantize kernel (one load per lane) is not capped.
-//   DISDP_XCD_CHUNK   0: block b takes tile b.  C > 0 (one tile per block):
-//                     the dispatcher deals blocks round-robin to the 8
-//                     XCDs, and XCD x takes the chunks x, x+8, x+16, ... of
-//                     C consecutive tiles, its blocks walking them in order.
-//                     -1: C = ceil(tiles / 8), one contiguous eighth of the
-//                     shard per XCD.
-#ifndef DISDP_UNROLL
-#define DISDP_UNROLL 1
-#endif
-#ifndef DISDP_GRID_MODE
-#define DISDP_GRID_MODE 1
-#endif
-#ifndef DISDP_GRID_ROUNDS
-#define DISDP_GRID_ROUNDS 1
-#endif
-#ifndef DISDP_NT
-#define DISDP_NT 3
-#endif
-#ifndef DISDP_BLOCK
-#define DISDP_BLOCK 64
-#endif
-#ifndef DISDP_QUANT_BLOCK
-#define DISDP_QUANT_BLOCK 64  // lanes per block of the quantize kernels
-#endif
-#ifndef DISDP_WAVE_CONTIG
-#define DISDP_WAVE_CONTIG 0
-#endif
-#ifndef DISDP_MIN_WAVES
-#define DISDP_MIN_WAVES 0
-#endif
-#ifndef DISDP_WAVES_PER_CU
-#define DISDP_WAVES_PER_CU 0
-#endif
-#ifndef DISDP_WAVES_PER_CU_FIXED
-#define DISDP_WAVES_PER_CU_FIXED 0
-#endif
-#ifndef DISDP_XCD_CHUNK
-#define DISDP_XCD_CHUNK 0
-#endif
-#if DISDP_XCD_CHUNK != 0 && DISDP_GRID_MODE != 1
-#error "DISDP_XCD_CHUNK needs one tile per block (DISDP_GRID_MODE=1)"
-#endif
-constexpr int kXcds = 8;
-#if DISDP_MIN_WAVES > 0
-#define DISDP_LAUNCH_BOUNDS __launch_bounds__(DISDP_BLOCK, DISDP_MIN_WAVES)
-#else
-#define DISDP_LAUNCH_BOUNDS __launch_bounds__(DISDP_BLOCK)
-#endif
-#define DISDP_QUANT_LAUNCH_BOUNDS __launch_bounds__(DISDP_QUANT_BLOCK)
+// The "shared" shape (four-wave blocks, one occupancy cap per mode) is for
+// a GPU whose compute kernels run on other streams at the same time: a
+// retiring four-wave block leaves a hole a compute workgroup can take, so
+// the chip is shared more evenly (see launch_shape below).
+#define DISDP_LAUNCH_BOUNDS __launch_bounds__(256)
+#define DISDP_WAVE_LAUNCH_BOUNDS __launch_bounds__(64)
 
 namespace disdp {
 namespace {
 
-constexpr int kBlock = DISDP_BLOCK;
-constexpr int kQuantBlock = DISDP_QUANT_BLOCK;
-// block 0 does the head elements (a loop over its lanes) and the 3 tail
-// elements (one per lane)
-static_assert(DISDP_BLOCK % 64 == 0 && DISDP_QUANT_BLOCK % 64 == 0,
-              "blocks are whole 64-lane waves");
 constexpr int kWave = 64;
+constexpr int kMaxBlock = 256;   // lanes per block of the shared shape
+// lanes per block of the many-tensor and quantize kernels (one wave)
+constexpr int kWaveBlock = kWave;
 
 // Vector types of the 4-element groups, declared only 4-byte aligned: a
 // group of an array that starts off its natural vector boundary (arrays with
@@ -131,23 +65,12 @@ typedef float f32x4 __attribute__((ext_vector_type(4), aligned(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2), aligned(4)));
 typedef int32_t i32x4 __attribute__((ext_vector_type(4), aligned(4)));
 
-// Non-temporal group loads and stores.  Overloads, not a template: deducing
-// the vector type would drop the typedef's 4-byte alignment.
-#define DISDP_NT_ACCESS(T)                                  \
-    __device__ __forceinline__ T ld_nt(const T *p)          \
-    {                                                       \
-        if constexpr (DISDP_NT & 1)                         \
-            return __builtin_nontemporal_load(p);           \
-        else                                                \
-            return *p;                                      \
-    }                                                       \
-    __device__ __forceinline__ void st_nt(T *p, T v)        \
-    {                                                       \
-        if constexpr (DISDP_NT & 2)                         \
-            __builtin_nontemporal_store(v, p);              \
-        else                                                \
-            *p = v;                                         \
-    }
+// Non-temporal group loads and stores (every byte is touched once).
+// Overloads, not a template: deducing the vector type would drop the
+// typedef's 4-byte alignment.
+#define DISDP_NT_ACCESS(T)                                                              \
+    __device__ __forceinline__ T ld_nt(const T *p) { return __builtin_nontemporal_load(p); } \
+    __device__ __forceinline__ void st_nt(T *p, T v) { __builtin_nontemporal_store(v, p); }
 DISDP_NT_ACCESS(f32x4)
 DISDP_NT_ACCESS(u32x2)
 DISDP_NT_ACCESS(i32x4)
@@ -339,41 +262,34 @@ __device__ __forceinline__ void finish_group(const A &a, int64_t grp, const floa
     }
 }
 
-// ---- U groups per lane, W known at compile time ---------------------------
+// ---- one group per lane, W known at compile time --------------------------
 
-// Groups g0, g0 + stride, ..., g0 + (U-1) stride: every load first, then
-// the arithmetic, then the stores.
-template <int W, int GT, int MODE, bool ADAM, int U, class A>
-__device__ __forceinline__ void process_groups(const A &a, int64_t g0, int stride)
+// Group `grp`: every load first, then the arithmetic, then the stores.
+template <int W, int GT, int MODE, bool ADAM, class A>
+__device__ __forceinline__ void process_group(const A &a, int64_t grp)
 {
-    typename Contrib<GT>::type c[U][W][4];
-    f32x4 P[U], M[U], V[U];
+    typename Contrib<GT>::type c[W][4];
+    f32x4 P{}, M{}, V{};
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-#pragma unroll
-        for (int w = 0; w < W; ++w)
-            load_group<GT>(a.g[w], g0 + u * stride, c[u][w]);
-        if constexpr (ADAM) {
-            P[u] = ld_nt(reinterpret_cast<const f32x4 *>(a.p) + g0 + u * stride);
-            M[u] = ld_nt(reinterpret_cast<const f32x4 *>(a.m) + g0 + u * stride);
-            V[u] = ld_nt(reinterpret_cast<const f32x4 *>(a.v) + g0 + u * stride);
-        }
+    for (int w = 0; w < W; ++w)
+        load_group<GT>(a.g[w], grp, c[w]);
+    if constexpr (ADAM) {
+        P = ld_nt(reinterpret_cast<const f32x4 *>(a.p) + grp);
+        M = ld_nt(reinterpret_cast<const f32x4 *>(a.m) + grp);
+        V = ld_nt(reinterpret_cast<const f32x4 *>(a.v) + grp);
     }
+    float agg[4];
+    int32_t ai[4];
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-        float agg[4];
-        int32_t ai[4];
+    for (int e = 0; e < 4; ++e) {
+        Acc<MODE> acc;
+        acc.first(c[0][e], a.qscale);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            Acc<MODE> acc;
-            acc.first(c[u][0][e], a.qscale);
-#pragma unroll
-            for (int w = 1; w < W; ++w)
-                acc.next(c[u][w][e], a.qscale);
-            agg[e] = acc.result(a.dqscale, ai[e]);
-        }
-        finish_group<MODE, ADAM>(a, g0 + u * stride, agg, ai, P[u], M[u], V[u]);
+        for (int w = 1; w < W; ++w)
+            acc.next(c[w][e], a.qscale);
+        agg[e] = acc.result(a.dqscale, ai[e]);
     }
+    finish_group<MODE, ADAM>(a, grp, agg, ai, P, M, V);
 }
 
 // ---- one group per lane, W known only at run time (W <= 64) ---------------
@@ -473,57 +389,23 @@ __device__ __forceinline__ void process_element(const A &a, int64_t i)
 
 // ---- kernels -----------------------------------------------------------------
 
-// Tiles per XCD chunk for a shard of `n_tiles` full tiles (>= 1).
-[[maybe_unused]] __host__ __device__ __forceinline__ int64_t xcd_chunk(int64_t n_tiles)
-{
-    if (DISDP_XCD_CHUNK > 0)
-        return DISDP_XCD_CHUNK;
-    const int64_t c = (n_tiles + kXcds - 1) / kXcds;
-    return c > 0 ? c : 1;
-}
-
-// Vector kernel.  W > 0: compile-time worker count, U groups per lane;
-// W == 0: run-time worker count, one group per lane.  Groups [0, n/4) go
-// grid-stride in tiles of kBlock*U groups; the groups after the last full
-// tile go one per lane; the last n % 4 elements and the a.head elements
-// before the (advanced) pointers go to lanes of block 0.  Every pointer is
-// on a 4-byte boundary; the front end chose the head.
-template <int W, int GT, int MODE, bool ADAM, int U>
+// Vector kernel.  W > 0: compile-time worker count; W == 0: run-time worker
+// count.  One 4-element group per lane, grid-stride over the groups [0,
+// n/4) (one pass when the grid covers the shard; a grid clamped to what one
+// dispatch counts walks on); the last n % 4 elements and the a.head
+// elements before the (advanced) pointers go to lanes of block 0.  Every
+// pointer is on a 4-byte boundary; the front end chose the head.  Block
+// size is the launch's (64 or 256 lanes).
+template <int W, int GT, int MODE, bool ADAM>
 __global__ DISDP_LAUNCH_BOUNDS void vector_kernel(LaunchArgs a)
 {
     const int64_t n_groups = a.n >> 2;
-    const int64_t tile = static_cast<int64_t>(kBlock) * U;
-    const int64_t n_tiles = n_groups / tile;
-#if DISDP_WAVE_CONTIG
-    const int lane_off = (threadIdx.x / kWave) * (kWave * U) + threadIdx.x % kWave;
-    constexpr int kStride = kWave;
-#else
-    const int lane_off = threadIdx.x;
-    constexpr int kStride = kBlock;
-#endif
-#if DISDP_XCD_CHUNK != 0
-    // one tile per block; block b is the j-th block of XCD x = b mod 8, and
-    // XCD x's j-th tile is tile j mod C of its (j / C)-th chunk, which is
-    // chunk (j / C) * 8 + x of the shard
-    const int64_t chunk = xcd_chunk(n_tiles);
-    const int64_t j = blockIdx.x / kXcds;
-    const int64_t t_first = ((j / chunk) * kXcds + blockIdx.x % kXcds) * chunk + j % chunk;
-    const int64_t t_end = t_first < n_tiles ? t_first + 1 : 0;
-    for (int64_t t = t_first; t < t_end; ++t) {
-#else
-    for (int64_t t = blockIdx.x; t < n_tiles; t += gridDim.x) {
-#endif
-        const int64_t g0 = t * tile + lane_off;
+    const int lanes = blockDim.x;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * lanes;
+    for (int64_t grp = static_cast<int64_t>(blockIdx.x) * lanes + threadIdx.x; grp < n_groups;
+         grp += stride) {
         if constexpr (W > 0)
-            process_groups<W, GT, MODE, ADAM, U>(a, g0, kStride);
-        else
-            process_group_rt<GT, MODE, ADAM>(a, g0);
-    }
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
-    for (int64_t grp = n_tiles * tile + static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-         grp < n_groups; grp += stride) {
-        if constexpr (W > 0)
-            process_groups<W, GT, MODE, ADAM, 1>(a, grp, kBlock);
+            process_group<W, GT, MODE, ADAM>(a, grp);
         else
             process_group_rt<GT, MODE, ADAM>(a, grp);
     }
@@ -531,7 +413,7 @@ __global__ DISDP_LAUNCH_BOUNDS void vector_kernel(LaunchArgs a)
         process_element<GT, MODE, ADAM>(a, (n_groups << 2) + threadIdx.x);
     // the elements before the advanced pointers
     if (blockIdx.x == 0)
-        for (int j = threadIdx.x; j < a.head; j += kBlock)
+        for (int j = threadIdx.x; j < a.head; j += lanes)
             process_element<GT, MODE, ADAM>(a, static_cast<int64_t>(j) - a.head);
 }
 
@@ -540,8 +422,9 @@ __global__ DISDP_LAUNCH_BOUNDS void vector_kernel(LaunchArgs a)
 template <int GT, int MODE, bool ADAM>
 __global__ DISDP_LAUNCH_BOUNDS void element_kernel(LaunchArgs a)
 {
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
-    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < a.n; i += stride)
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < a.n;
+         i += stride)
         process_element<GT, MODE, ADAM>(a, i);
 }
 
@@ -567,7 +450,7 @@ struct TensorView {
 // vector_kernel: whole groups one per lane, the last n % 4 elements by the
 // tensor's last tile, its head elements by its first tile.
 template <int W, int GT, int MODE>
-__global__ DISDP_LAUNCH_BOUNDS void multi_kernel(MultiArgs ma)
+__global__ DISDP_WAVE_LAUNCH_BOUNDS void multi_kernel(MultiArgs ma)
 {
     const int64_t total = ma.tile_start[ma.count];
     const int per_tensor = ma.W + 4;
@@ -598,11 +481,11 @@ __global__ DISDP_LAUNCH_BOUNDS void multi_kernel(MultiArgs ma)
         const int64_t n = ma.n[j];
         const int64_t n_groups = n >> 2;
         const int64_t tile = vb - ma.tile_start[j];
-        for (int l = threadIdx.x; l < kMultiTileGroups; l += kBlock) {
+        for (int l = threadIdx.x; l < kMultiTileGroups; l += kWaveBlock) {
             const int64_t grp = tile * kMultiTileGroups + l;
             if (grp < n_groups) {
                 if constexpr (W > 0)
-                    process_groups<W, GT, MODE, true, 1>(t, grp, kBlock);
+                    process_group<W, GT, MODE, true>(t, grp);
                 else
                     process_group_rt<GT, MODE, true>(t, grp);
             }
@@ -610,7 +493,7 @@ __global__ DISDP_LAUNCH_BOUNDS void multi_kernel(MultiArgs ma)
         if (vb == ma.tile_start[j + 1] - 1 && threadIdx.x < (n & 3))
             process_element<GT, MODE, true>(t, (n_groups << 2) + threadIdx.x);
         if (tile == 0)
-            for (int e = threadIdx.x; e < ma.head[j]; e += kBlock)
+            for (int e = threadIdx.x; e < ma.head[j]; e += kWaveBlock)
                 process_element<GT, MODE, true>(t, static_cast<int64_t>(e) - ma.head[j]);
     }
 }
@@ -618,14 +501,14 @@ __global__ DISDP_LAUNCH_BOUNDS void multi_kernel(MultiArgs ma)
 // ---- the format conversion as a producer ------------------------------------
 
 // out = quantize(g) over 4-element groups (one group per lane, grid-stride
-// over kQuantBlock-lane blocks), the last n % 4 and the head elements by
+// over kWaveBlock-lane blocks), the last n % 4 and the head elements by
 // block 0.
 template <int GT>
-__global__ DISDP_QUANT_LAUNCH_BOUNDS void quantize_vector_kernel(QuantizeArgs q)
+__global__ DISDP_WAVE_LAUNCH_BOUNDS void quantize_vector_kernel(QuantizeArgs q)
 {
     const int64_t n_groups = q.n >> 2;
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * kQuantBlock;
-    for (int64_t grp = static_cast<int64_t>(blockIdx.x) * kQuantBlock + threadIdx.x; grp < n_groups;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kWaveBlock;
+    for (int64_t grp = static_cast<int64_t>(blockIdx.x) * kWaveBlock + threadIdx.x; grp < n_groups;
          grp += stride) {
         float x[4];
         load_group<GT>(q.g, grp, x);
@@ -638,23 +521,21 @@ __global__ DISDP_QUANT_LAUNCH_BOUNDS void quantize_vector_kernel(QuantizeArgs q)
         q.out[i] = quantize(load_one<GT>(q.g, i), q.qscale);
     }
     if (blockIdx.x == 0)
-        for (int j = threadIdx.x; j < q.head; j += kQuantBlock) {
+        for (int j = threadIdx.x; j < q.head; j += kWaveBlock) {
             const int64_t i = static_cast<int64_t>(j) - q.head;
             q.out[i] = quantize(load_one<GT>(q.g, i), q.qscale);
         }
 }
 
 template <int GT>
-__global__ DISDP_QUANT_LAUNCH_BOUNDS void quantize_element_kernel(QuantizeArgs q)
+__global__ DISDP_WAVE_LAUNCH_BOUNDS void quantize_element_kernel(QuantizeArgs q)
 {
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * kQuantBlock;
-    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kQuantBlock + threadIdx.x; i < q.n; i += stride)
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kWaveBlock;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kWaveBlock + threadIdx.x; i < q.n; i += stride)
         q.out[i] = quantize(load_one<GT>(q.g, i), q.qscale);
 }
 
 // ---- host side: grid sizing and dispatch --------------------------------------
-
-constexpr int kU = DISDP_UNROLL;
 
 // Resident waves per CU for a fixed-point kernel converting float
 // contributions, by the bytes of loads a lane keeps in flight, as in fp32
@@ -670,8 +551,6 @@ constexpr int kU = DISDP_UNROLL;
 // caps.
 constexpr int fixed_mode_waves(int lane_bytes, bool bf16)
 {
-    if (DISDP_WAVES_PER_CU_FIXED > 0)
-        return DISDP_WAVES_PER_CU_FIXED;
     return lane_bytes <= 80 ? 14 : lane_bytes <= 112 ? 12 : bf16 ? 10 : lane_bytes <= 176 ? 8 : 6;
 }
 
@@ -683,8 +562,6 @@ constexpr int fixed_mode_waves(int lane_bytes, bool bf16)
 // 176 B (fp32 W = 5-8, bf16 W = 12, 16), 6 beyond (fp32 W = 12, 16).
 constexpr int fp32_mode_waves(int lane_bytes)
 {
-    if (DISDP_WAVES_PER_CU != 0)
-        return DISDP_WAVES_PER_CU > 0 ? DISDP_WAVES_PER_CU : 0;
     return lane_bytes <= 112 ? 12 : lane_bytes <= 176 ? 8 : 6;
 }
 
@@ -701,15 +578,41 @@ int runtime_w_waves(int W, int gt, int mode)
 {
     const bool bf16 = gt == kGradBF16;
     const int chunk = bf16 ? 16 : 8;
-    if (mode == kAggFixed && gt != kGradI32) {
-        if (DISDP_WAVES_PER_CU_FIXED > 0)
-            return DISDP_WAVES_PER_CU_FIXED;
+    if (mode == kAggFixed && gt != kGradI32)
         return (W % chunk ? 10 : 8) + (bf16 ? 2 : 0);
-    }
-    if (DISDP_WAVES_PER_CU != 0)
-        return DISDP_WAVES_PER_CU > 0 ? DISDP_WAVES_PER_CU : 0;
     return W < chunk ? 14 : W % chunk ? 10 : 8;
 }
+
+// The launch shape of the vector kernels for one call.
+//   solo   (default): one-wave blocks, occupancy caps from the tables above
+//          -- the fastest shape when the kernel has the GPU to itself.
+//   shared (DISDP_LAUNCH_SHAPE=shared in the environment): four-wave blocks
+//          capped at 12 waves per CU, 20 for fixed-point kernels that
+//          convert float contributions.  Next to a bf16 GEMM loop on
+//          another stream of the same (unmasked) GPU, the solo shape's
+//          stream of one-wave blocks refills every slot a retiring block
+//          frees and the GEMM slows about 10x while the fused call slows
+//          1.1x; a retiring four-wave block leaves a hole of four wave slots
+//          that a GEMM workgroup can take, and the two slow each other about
+//          evenly (measured 1.7x and 2.0x), at 3-5% below the solo shape's
+//          rate when alone.
+// The variable is read on every call, so a process can switch between
+// calls; any other value means solo.
+struct Shape {
+    int lanes;        // lanes per block
+    bool shared;
+};
+
+Shape launch_shape()
+{
+    const char *s = std::getenv("DISDP_LAUNCH_SHAPE");
+    if (s && std::strcmp(s, "shared") == 0)
+        return Shape{kMaxBlock, true};
+    return Shape{kWave, false};
+}
+
+constexpr int kSharedWaves = 12;
+constexpr int kSharedWavesConverting = 20;
 
 // Dynamic LDS bytes a vector-kernel block reserves so that at most
 // `blocks_per_cu` blocks fit on a CU (0 = no cap), cached per device.
@@ -761,15 +664,20 @@ int cu_count()
 
 // CUs `stream` may run on: the number of bits of its CU mask among the
 // device's CUs (hipExtStreamCreateWithCUMask), or all of them when the
-// runtime cannot say.
+// runtime cannot say.  An error the query records is cleared only when no
+// error was pending before it, so a caller's own pending error survives.
 int stream_cus(hipStream_t stream)
 {
     const int total = cu_count();
     constexpr int kMaxWords = 32;  // masks of up to 1024 CUs
     const int words = (total + 31) / 32;
     uint32_t mask[kMaxWords] = {};
-    if (words > kMaxWords || hipExtStreamGetCUMask(stream, words, mask) != hipSuccess) {
-        (void)hipGetLastError();  // clear the error the query recorded
+    if (words > kMaxWords)
+        return total;
+    const hipError_t pending = hipPeekAtLastError();
+    if (hipExtStreamGetCUMask(stream, words, mask) != hipSuccess) {
+        if (pending == hipSuccess)
+            (void)hipGetLastError();
         return total;
     }
     int c = 0;
@@ -778,18 +686,16 @@ int stream_cus(hipStream_t stream)
     return c > 0 ? c : total;
 }
 
-// Resident-block cap per CU for a launch on `stream`: `base_waves` is the
-// cap in waves for the whole chip.  What streams best is a number of
-// resident waves chip-wide, so on a stream restricted to fewer CUs each CU
-// takes proportionally more, up to kMaxScaledWaves (the register limit of
-// the W = 8 kernels).  Measured on the 7B/8 shard with 32 / 64 / 128 CUs:
-// 20 waves per CU streamed 41% / 35% / 19% faster than the full-chip cap
-// of the time (12 waves per CU, in 4-wave blocks).
-#ifndef DISDP_MAX_SCALED_WAVES
-#define DISDP_MAX_SCALED_WAVES 20
-#endif
-constexpr int kMaxScaledWaves = DISDP_MAX_SCALED_WAVES;
-int blocks_per_cu_cap(int base_waves, hipStream_t stream)
+// Resident-block cap per CU for a launch of `lanes`-lane blocks on
+// `stream`: `base_waves` is the cap in waves for the whole chip.  What
+// streams best is a number of resident waves chip-wide, so on a stream
+// restricted to fewer CUs each CU takes proportionally more, up to
+// kMaxScaledWaves (the register limit of the W = 8 kernels).  Measured on
+// the 7B/8 shard with 32 / 64 / 128 CUs: 20 waves per CU streamed 41% / 35%
+// / 19% faster than the full-chip cap of the time (12 waves per CU, in
+// 4-wave blocks).
+constexpr int kMaxScaledWaves = 20;
+int blocks_per_cu_cap(int base_waves, int lanes, hipStream_t stream)
 {
     if (base_waves <= 0)
         return 0;
@@ -801,37 +707,8 @@ int blocks_per_cu_cap(int base_waves, hipStream_t stream)
         waves = scaled < kMaxScaledWaves ? scaled
                                          : (base_waves > kMaxScaledWaves ? base_waves : kMaxScaledWaves);
     }
-    constexpr int kWavesPerBlock = kBlock / kWave;
-    const int blocks = waves / kWavesPerBlock;
+    const int blocks = waves / (lanes / kWave);
     return blocks > 0 ? blocks : 1;
-}
-
-// Blocks of `fn` that fit on one CU at once (registers, or the reserved
-// LDS), cached per (kernel, LDS reservation).  Occupancy depends only on
-// the kernel, the block size and the reservation, so one entry serves every
-// device of one architecture.
-int resident_blocks_per_cu(const void *fn, int lds_bytes)
-{
-    static std::mutex mu;
-    static const void *keys[512];
-    static int key_lds[512];
-    static int vals[512];
-    static int used = 0;
-    std::lock_guard<std::mutex> lock(mu);
-    for (int i = 0; i < used; ++i)
-        if (keys[i] == fn && key_lds[i] == lds_bytes)
-            return vals[i];
-    int nb = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, fn, kBlock, lds_bytes) != hipSuccess ||
-        nb < 1)
-        nb = 1;
-    if (used < 512) {
-        keys[used] = fn;
-        key_lds[used] = lds_bytes;
-        vals[used] = nb;
-        ++used;
-    }
-    return nb;
 }
 
 int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -839,8 +716,7 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 // A dispatch counts its work-items in 32 bits per dimension, so a grid of
 // `block`-lane blocks holds at most (2^32 - 1) / block of them.  Every
 // kernel here walks its work grid-stride, so a clamped grid still covers a
-// shard of any accepted size (beyond 2^34 elements for the one-tile-per-
-// block grids).
+// shard of any accepted size.
 constexpr int64_t kMaxGridLanes = 0xffffffffLL;
 int64_t clamp_grid(int64_t blocks, int block)
 {
@@ -848,98 +724,92 @@ int64_t clamp_grid(int64_t blocks, int block)
     return blocks < 1 ? 1 : blocks > max_blocks ? max_blocks : blocks;
 }
 
-// `work_blocks`: blocks needed for one tile (or element chunk) each;
-// `lds_bytes`: dynamic LDS reserved per block (an occupancy cap).
-hipError_t launch_kernel(const void *fn, int64_t work_blocks, bool persistent, const LaunchArgs &a,
+// `blocks` blocks of `lanes` lanes (clamped), `lds_bytes` of dynamic LDS
+// reserved per block (an occupancy cap).
+hipError_t launch_kernel(const void *fn, int64_t blocks, int lanes, const LaunchArgs &a,
                          hipStream_t stream, int lds_bytes = 0)
 {
-    int64_t blocks = work_blocks;
-    if (persistent) {
-        const int64_t cap = static_cast<int64_t>(cu_count()) * resident_blocks_per_cu(fn, lds_bytes) *
-                            DISDP_GRID_ROUNDS;
-        if (blocks > cap)
-            blocks = cap;
-    }
-    blocks = clamp_grid(blocks, kBlock);
+    blocks = clamp_grid(blocks, lanes);
     void *args[] = {const_cast<LaunchArgs *>(&a)};
-    return hipLaunchKernel(fn, dim3(static_cast<unsigned>(blocks)), dim3(kBlock), args,
+    return hipLaunchKernel(fn, dim3(static_cast<unsigned>(blocks)), dim3(lanes), args,
                            static_cast<size_t>(lds_bytes), stream);
 }
 
 template <int W, int GT, int MODE, bool ADAM>
-hipError_t launch_vector(const LaunchArgs &a, hipStream_t stream)
+hipError_t launch_vector(const LaunchArgs &a, Shape shape, hipStream_t stream)
 {
-    constexpr int U = W > 0 ? kU : 1;
-    const int64_t n_groups = a.n >> 2;
-    int64_t blocks = ceil_div(n_groups, static_cast<int64_t>(kBlock) * U);
-#if DISDP_XCD_CHUNK != 0
-    // every XCD gets ceil(chunks / 8) chunks of C blocks; the ragged groups
-    // after the last full tile go to the grid-stride loop of all blocks
-    {
-        const int64_t n_tiles = n_groups / (static_cast<int64_t>(kBlock) * U);
-        const int64_t c = xcd_chunk(n_tiles);
-        blocks = kXcds * ceil_div(ceil_div(n_tiles, c), kXcds) * c;
-        // this tile order is not grid-stride: a clamped grid would skip tiles
-        if (blocks != clamp_grid(blocks, kBlock))
-            return hipErrorInvalidConfiguration;
-    }
-#endif
+    const int64_t blocks = ceil_div(a.n >> 2, shape.lanes);
     // bytes of loads one lane keeps in flight: 4 elements of each
     // contribution, plus p, m and v with the optimizer (run-time W: many)
     constexpr int kGradBytes = GT == kGradBF16 ? 2 : 4;
     constexpr int kLaneBytes = W > 0 ? 4 * (W * kGradBytes + (ADAM ? 12 : 0)) : 1 << 30;
     constexpr bool kConverts = MODE == kAggFixed && GT != kGradI32;
-    const int base = W == 0    ? runtime_w_waves(a.W, GT, MODE)
-                     : kConverts ? fixed_mode_waves(kLaneBytes, GT == kGradBF16)
-                                 : fp32_mode_waves(kLaneBytes);
-    return launch_kernel(reinterpret_cast<const void *>(&vector_kernel<W, GT, MODE, ADAM, U>),
-                         blocks, DISDP_GRID_MODE == 0, a, stream,
-                         occupancy_lds_bytes(blocks_per_cu_cap(base, stream)));
+    int base;
+    if (shape.shared)
+        base = kConverts ? kSharedWavesConverting : kSharedWaves;
+    else
+        base = W == 0      ? runtime_w_waves(a.W, GT, MODE)
+               : kConverts ? fixed_mode_waves(kLaneBytes, GT == kGradBF16)
+                           : fp32_mode_waves(kLaneBytes);
+    return launch_kernel(reinterpret_cast<const void *>(&vector_kernel<W, GT, MODE, ADAM>), blocks,
+                         shape.lanes, a, stream,
+                         occupancy_lds_bytes(blocks_per_cu_cap(base, shape.lanes, stream)));
 }
 
+// The element kernel walks the shard grid-stride with 32 waves per CU (its
+// registers allow that many resident).
+constexpr int kElementWavesPerCu = 32;
+
 template <int GT, int MODE, bool ADAM>
-hipError_t dispatch_w(const LaunchArgs &a, bool vec, hipStream_t stream)
+hipError_t dispatch_w(const LaunchArgs &a, bool vec, Shape shape, hipStream_t stream)
 {
-    if (!vec)
+    if (!vec) {
+        const int64_t cap = static_cast<int64_t>(cu_count()) * kElementWavesPerCu /
+                            (shape.lanes / kWave);
+        const int64_t need = ceil_div(a.n, shape.lanes);
         return launch_kernel(reinterpret_cast<const void *>(&element_kernel<GT, MODE, ADAM>),
-                             ceil_div(a.n, kBlock), /*persistent=*/true, a, stream);
+                             need < cap ? need : cap, shape.lanes, a, stream);
+    }
     switch (a.W) {
-    case 1: return launch_vector<1, GT, MODE, ADAM>(a, stream);
-    case 2: return launch_vector<2, GT, MODE, ADAM>(a, stream);
-    case 3: return launch_vector<3, GT, MODE, ADAM>(a, stream);
-    case 4: return launch_vector<4, GT, MODE, ADAM>(a, stream);
-    case 5: return launch_vector<5, GT, MODE, ADAM>(a, stream);
-    case 6: return launch_vector<6, GT, MODE, ADAM>(a, stream);
-    case 7: return launch_vector<7, GT, MODE, ADAM>(a, stream);
-    case 8: return launch_vector<8, GT, MODE, ADAM>(a, stream);
-    case 12: return launch_vector<12, GT, MODE, ADAM>(a, stream);
-    case 16: return launch_vector<16, GT, MODE, ADAM>(a, stream);
-    default: return launch_vector<0, GT, MODE, ADAM>(a, stream);
+    case 1: return launch_vector<1, GT, MODE, ADAM>(a, shape, stream);
+    case 2: return launch_vector<2, GT, MODE, ADAM>(a, shape, stream);
+    case 3: return launch_vector<3, GT, MODE, ADAM>(a, shape, stream);
+    case 4: return launch_vector<4, GT, MODE, ADAM>(a, shape, stream);
+    case 5: return launch_vector<5, GT, MODE, ADAM>(a, shape, stream);
+    case 6: return launch_vector<6, GT, MODE, ADAM>(a, shape, stream);
+    case 7: return launch_vector<7, GT, MODE, ADAM>(a, shape, stream);
+    case 8: return launch_vector<8, GT, MODE, ADAM>(a, shape, stream);
+    case 12: return launch_vector<12, GT, MODE, ADAM>(a, shape, stream);
+    case 16: return launch_vector<16, GT, MODE, ADAM>(a, shape, stream);
+    default: return launch_vector<0, GT, MODE, ADAM>(a, shape, stream);
     }
 }
 
 template <bool ADAM>
-hipError_t dispatch(const LaunchArgs &a, bool vec, hipStream_t stream)
+hipError_t dispatch(const LaunchArgs &a, bool vec, Shape shape, hipStream_t stream)
 {
     if (a.gdtype == kGradI32)  // the front end admits int32 only in fixed mode
-        return dispatch_w<kGradI32, kAggFixed, ADAM>(a, vec, stream);
+        return dispatch_w<kGradI32, kAggFixed, ADAM>(a, vec, shape, stream);
     if (a.gdtype == kGradF32)
-        return a.mode == kAggFP32 ? dispatch_w<kGradF32, kAggFP32, ADAM>(a, vec, stream)
-                                  : dispatch_w<kGradF32, kAggFixed, ADAM>(a, vec, stream);
-    return a.mode == kAggFP32 ? dispatch_w<kGradBF16, kAggFP32, ADAM>(a, vec, stream)
-                              : dispatch_w<kGradBF16, kAggFixed, ADAM>(a, vec, stream);
+        return a.mode == kAggFP32 ? dispatch_w<kGradF32, kAggFP32, ADAM>(a, vec, shape, stream)
+                                  : dispatch_w<kGradF32, kAggFixed, ADAM>(a, vec, shape, stream);
+    return a.mode == kAggFP32 ? dispatch_w<kGradBF16, kAggFP32, ADAM>(a, vec, shape, stream)
+                              : dispatch_w<kGradBF16, kAggFixed, ADAM>(a, vec, shape, stream);
 }
 
 }  // namespace
 
 hipError_t launch(const LaunchArgs &a, Kind kind, bool vector_path, hipStream_t stream)
 {
-    return kind == kAggregateAdam ? dispatch<true>(a, vector_path, stream)
-                                  : dispatch<false>(a, vector_path, stream);
+    const Shape shape = launch_shape();
+    return kind == kAggregateAdam ? dispatch<true>(a, vector_path, shape, stream)
+                                  : dispatch<false>(a, vector_path, shape, stream);
 }
 
 namespace {
 
+// The many-tensor kernel always runs one-wave blocks: its virtual block is
+// one 64-group tile.
 template <int W, int GT, int MODE>
 hipError_t launch_multi_w(const MultiArgs &a, hipStream_t stream)
 {
@@ -949,11 +819,11 @@ hipError_t launch_multi_w(const MultiArgs &a, hipStream_t stream)
     const int base = W == 0    ? runtime_w_waves(a.W, GT, MODE)
                      : kConverts ? fixed_mode_waves(kLaneBytes, GT == kGradBF16)
                                  : fp32_mode_waves(kLaneBytes);
-    const int lds = occupancy_lds_bytes(blocks_per_cu_cap(base, stream));
-    const int64_t blocks = clamp_grid(a.tile_start[a.count], kBlock);
+    const int lds = occupancy_lds_bytes(blocks_per_cu_cap(base, kWaveBlock, stream));
+    const int64_t blocks = clamp_grid(a.tile_start[a.count], kWaveBlock);
     void *args[] = {const_cast<MultiArgs *>(&a)};
     return hipLaunchKernel(reinterpret_cast<const void *>(&multi_kernel<W, GT, MODE>),
-                           dim3(static_cast<unsigned>(blocks)), dim3(kBlock), args,
+                           dim3(static_cast<unsigned>(blocks)), dim3(kWaveBlock), args,
                            static_cast<size_t>(lds), stream);
 }
 
@@ -995,15 +865,15 @@ hipError_t launch_quantize(const QuantizeArgs &q, bool vector_path, hipStream_t 
     if (vector_path) {
         fn = q.gdtype == kGradBF16 ? reinterpret_cast<const void *>(&quantize_vector_kernel<kGradBF16>)
                                    : reinterpret_cast<const void *>(&quantize_vector_kernel<kGradF32>);
-        blocks = ceil_div(q.n >> 2, kQuantBlock);
+        blocks = ceil_div(q.n >> 2, kWaveBlock);
     } else {
         fn = q.gdtype == kGradBF16 ? reinterpret_cast<const void *>(&quantize_element_kernel<kGradBF16>)
                                    : reinterpret_cast<const void *>(&quantize_element_kernel<kGradF32>);
-        blocks = ceil_div(q.n, kQuantBlock);
+        blocks = ceil_div(q.n, kWaveBlock);
     }
-    blocks = clamp_grid(blocks, kQuantBlock);
+    blocks = clamp_grid(blocks, kWaveBlock);
     void *args[] = {const_cast<QuantizeArgs *>(&q)};
-    return hipLaunchKernel(fn, dim3(static_cast<unsigned>(blocks)), dim3(kQuantBlock), args, 0,
+    return hipLaunchKernel(fn, dim3(static_cast<unsigned>(blocks)), dim3(kWaveBlock), args, 0,
                            stream);
 }
 

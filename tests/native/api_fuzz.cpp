@@ -99,6 +99,7 @@ extern "C" hipError_t hipMemGetAddressRange(hipDeviceptr_t *base, size_t *size, 
 }
 
 extern "C" hipError_t hipGetLastError(void) { return hipSuccess; }
+extern "C" hipError_t hipPeekAtLastError(void) { return hipSuccess; }
 
 // ---- helpers ------------------------------------------------------------------
 namespace {
