@@ -131,3 +131,79 @@ def run_fused_case(W, gdtype, mode, n, t=3, frac_bits=24, offsets=(0, 0),
                         want_agg_f32=want_agg, want_agg_i32=(want_agg and mode == "fixed"),
                         **hp)
     return got, want
+
+
+def host_threads() -> int:
+    """Host threads a test may use (the CPU share of one GPU: at most 16)."""
+    import os
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+def whole_shard_mismatches(grads, pre, post, *, gdtype, mode, frac_bits, t, hp,
+                           chunk=1 << 26, threads=None, label=""):
+    """Every element of one fused step against the oracle.
+
+    grads: the W contributions the step read (device tensors); pre: (p, m, v)
+    before the step (device copies); post: dict of the step's outputs
+    (device tensors) with keys p, m, v, p16 and optionally agg_i32.  The
+    shard is read back in chunks of `chunk` elements into pinned host
+    buffers; each chunk is split over `threads` host threads, each running
+    the C oracle on its piece and counting the elements whose bits differ.
+    Returns {output: mismatching elements}, plus "elements"."""
+    import time
+    from concurrent.futures import ThreadPoolExecutor
+    t_ = torch()
+    threads = threads or host_threads()
+    n = post["p"].numel()
+    keys = [k for k in ("p", "m", "v", "p16", "agg_i32") if k in post]
+    arrays = {f"g{w}": g for w, g in enumerate(grads)}
+    arrays.update({"p0": pre[0], "m0": pre[1], "v0": pre[2]})
+    arrays.update(post)
+    size = min(chunk, n)
+    pin = t_.cuda.is_available()
+    host = {k: t_.empty(size, dtype=a.dtype, pin_memory=pin) for k, a in arrays.items()}
+    bad = {k: 0 for k in keys}
+    oracle_mode = oracle.AGG_FIXED if mode == "fixed" else oracle.AGG_FP32
+    W = len(grads)
+
+    def piece(views, lo, hi):
+        gs = [views[f"g{w}"][lo:hi] for w in range(W)]
+        want = oracle.fused(gs, views["p0"][lo:hi], views["m0"][lo:hi], views["v0"][lo:hi],
+                            mode=oracle_mode, frac_bits=frac_bits, t=t,
+                            want_agg_i32="agg_i32" in keys, **hp)
+        out = {}
+        for k in keys:
+            g = views[k][lo:hi]
+            w_ = want[k]
+            if g.dtype == np.float32:
+                g, w_ = g.view(np.uint32), w_.view(np.uint32)
+            out[k] = int(np.count_nonzero(g != w_))
+        return out
+
+    t_copy = t_orc = 0.0
+    with ThreadPoolExecutor(max_workers=threads) as pool:
+        for s in range(0, n, size):
+            e = min(n, s + size)
+            c0 = time.perf_counter()
+            views = {}
+            for k, a in arrays.items():
+                h = host[k][:e - s]
+                h.copy_(a[s:e])
+                x = h.numpy()
+                views[k] = x.view(np.uint16) if x.dtype == np.int16 else x
+            c1 = time.perf_counter()
+            cuts = [(e - s) * j // threads for j in range(threads + 1)]
+            for res in pool.map(lambda j: piece(views, cuts[j], cuts[j + 1]), range(threads)):
+                for k, c in res.items():
+                    bad[k] += c
+            c2 = time.perf_counter()
+            t_copy += c1 - c0
+            t_orc += c2 - c1
+    print(f"[wholeshard] {label} {n} elements: read back {t_copy:.1f} s, oracle and "
+          f"compare {t_orc:.1f} s on {threads} threads; mismatches {bad}", flush=True)
+    bad["elements"] = n
+    return bad
