@@ -179,10 +179,15 @@ def host_threads() -> int:
 
 def cpu_baseline(wl, dg, dp, dm, dv, threads=1):
     """The oracle on the first CPU_SAMPLE elements of the same shard for
-    CPU_STEPS consecutive steps.  threads > 1 splits the sample into that
-    many contiguous chunks, one oracle call per chunk and step on a thread
-    pool (the calls release the interpreter lock), as the paper's parameter
-    server spreads its CPU Adam over threads."""
+    CPU_STEPS consecutive steps, each step updating p, m, v and the bf16
+    copy in place (buffers read back and allocated before the clock
+    starts).  threads > 1 splits the sample into that many contiguous
+    chunks, one oracle call per chunk and step on a thread pool (the calls
+    release the interpreter lock), as the paper's parameter server spreads
+    its CPU Adam over threads.  The oracle's loop streams its arrays once per
+    step with no reuse, so its per-element rate does not depend on the
+    length once the arrays are far beyond the host's caches (the 2^26-element
+    sample is 3.9 GB)."""
     import numpy as np
     import oracle
     from concurrent.futures import ThreadPoolExecutor
@@ -191,18 +196,18 @@ def cpu_baseline(wl, dg, dp, dm, dv, threads=1):
     for g in dg:
         a = g[:ns].cpu().numpy()
         gs.append(a.view(np.uint16) if wl.gdtype == "bf16" else a)
-    p, m, v = (x[:ns].cpu().numpy() for x in (dp, dm, dv))
+    p, m, v = (x[:ns].cpu().numpy().copy() for x in (dp, dm, dv))
+    p16 = np.zeros(ns, np.uint16)
     hp = hparams(wl)
     mode = oracle.AGG_FIXED if wl.mode == "fixed" else oracle.AGG_FP32
     cuts = [ns * k // threads for k in range(threads + 1)]
     chunks = [(lo, hi) for lo, hi in zip(cuts[:-1], cuts[1:]) if hi > lo]
-    state = [(p[lo:hi], m[lo:hi], v[lo:hi]) for lo, hi in chunks]
+    pieces = [([g[lo:hi] for g in gs], p[lo:hi], m[lo:hi], v[lo:hi], p16[lo:hi])
+              for lo, hi in chunks]
 
     def one(k, t):
-        lo, hi = chunks[k]
-        out = oracle.fused([g[lo:hi] for g in gs], *state[k], mode=mode,
-                           frac_bits=wl.frac_bits, t=t, **hp)
-        state[k] = (out["p"], out["m"], out["v"])
+        g, pk, mk, vk, ck = pieces[k]
+        oracle.fused_inplace(g, pk, mk, vk, ck, mode=mode, frac_bits=wl.frac_bits, t=t, **hp)
 
     with ThreadPoolExecutor(max_workers=len(chunks)) as pool:
         t0 = time.perf_counter()
@@ -212,8 +217,10 @@ def cpu_baseline(wl, dg, dp, dm, dv, threads=1):
     how = "single-threaded" if len(chunks) == 1 else f"{len(chunks)} threads, one chunk each"
     return {"value": round(ns * CPU_STEPS / dt / 1e9, 5),
             "unit": "G params/s", "cores": len(chunks), "kind": "oracle",
-            "sample": f"first {ns} elements of the shard, {CPU_STEPS} consecutive "
-                      f"steps, C oracle (gcc -O2), {how}, "
+            "sample_fraction": round(ns / wl.n, 4),
+            "sample": f"first {ns:,} of the shard's {wl.n:,} elements "
+                      f"({100 * ns / wl.n:.1f}%), {CPU_STEPS} consecutive steps, in place, "
+                      f"C oracle (gcc -O2), {how}, "
                       f"{dt:.1f} s on {host_cpu_model()} "
                       f"({os.cpu_count()} host threads visible)"}
 
@@ -340,11 +347,55 @@ def run_bench(args):
     print(json.dumps(line), flush=True)
 
 
+# PCIe 5.0 x16 (MI355X's host interface): 32 GT/s per lane, 16 lanes, per
+# direction, before the 128b/130b encoding.
+HOST_LINK_PEAK_GBPS = 64.0
+
+
+def host_link_probe(nbytes=1 << 32, reps=5):
+    """Host-link rates on this machine, GB/s per direction, median of `reps`:
+    DMA copies between pinned host memory and HBM (torch's copy engine
+    path), and the same bytes moved by the library's own kernel reading or
+    writing pinned host memory in place (disdp_aggregate of one fp32
+    contribution is a copy), the way the fused kernel reaches host state."""
+    import numpy as np
+    import torch
+    import paper_2409_00918_amd as dd
+    n = nbytes // 4
+    host = torch.ones(n, dtype=torch.float32, pin_memory=True)
+    dev = torch.empty(n, dtype=torch.float32, device="cuda")
+    s = torch.cuda.current_stream()
+
+    def rate(fn):
+        fn()
+        torch.cuda.synchronize()
+        ms = []
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(s)
+            fn()
+            b.record(s)
+            torch.cuda.synchronize()
+            ms.append(a.elapsed_time(b))
+        return round(nbytes / (float(np.median(ms)) * 1e-3) / 1e9, 1)
+
+    out = {"dma_h2d_GBps": rate(lambda: dev.copy_(host, non_blocking=True)),
+           "dma_d2h_GBps": rate(lambda: host.copy_(dev, non_blocking=True)),
+           "kernel_read_host_GBps": rate(lambda: dd.aggregate([host], agg_out_f32=dev)),
+           "kernel_write_host_GBps": rate(lambda: dd.aggregate([dev], agg_out_f32=host)),
+           "bytes_per_probe": nbytes}
+    del host, dev
+    torch.cuda.empty_cache()
+    return out
+
+
 def run_host_state(args):
     """Out-of-core shard: p, m, v and the bf16 copy in pinned host DRAM (as
     the paper's parameter server keeps its 12-byte states off the
     accelerator), W contributions in HBM.  The fused kernel streams the
-    state over the host link: 12 bytes in and 14 bytes out per element."""
+    state over the host link: 12 bytes in and 14 bytes out per element.
+    The line also carries the host link's measured rates (host_link_probe)
+    and its published peak."""
     import numpy as np
     import torch
     import paper_2409_00918_amd as dd
@@ -352,6 +403,7 @@ def run_host_state(args):
     wl = synth.WORKLOADS[args.workload]
     torch.cuda.set_device(0)
     dd.lib()
+    probe = host_link_probe()
     dg = synth.device_grads(wl.wid, 1, wl.W, wl.n, wl.sigma, gdtype=wl.gdtype,
                             outlier_frac=wl.outlier_frac, outlier_scale=wl.outlier_scale)
     dp, dm, dv = synth.device_state(wl.wid, wl.n, wl.p_sigma)
@@ -385,7 +437,8 @@ def run_host_state(args):
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
-    link = wl.n * (12 + 14) / (ms * 1e-3) / 1e9
+    h2d = wl.n * 12 / (ms * 1e-3) / 1e9
+    d2h = wl.n * 14 / (ms * 1e-3) / 1e9
     print(json.dumps({"metric": "G params/s aggregated+updated, state in pinned host memory",
                       "value": round(wl.n / (wall / args.steps) / 1e9, 3), "unit": "G params/s",
                       "ms_per_step": round(wall * 1e3 / args.steps, 3),
@@ -393,10 +446,14 @@ def run_host_state(args):
                       "config": {"workload": wl.name, "n": wl.n, "W": wl.W,
                                  "state": "pinned host (hipHostMalloc), streamed by the kernel",
                                  "contributions": "HBM"},
-                      "host_link": {"achieved_GBps_both_directions": round(link, 1),
-                                    "h2d_GBps": round(wl.n * 12 / (ms * 1e-3) / 1e9, 1),
-                                    "d2h_GBps": round(wl.n * 14 / (ms * 1e-3) / 1e9, 1),
-                                    "bytes_per_element": {"h2d": 12, "d2h": 14}}}),
+                      "host_link": {"achieved_GBps_both_directions": round(h2d + d2h, 1),
+                                    "h2d_GBps": round(h2d, 1), "d2h_GBps": round(d2h, 1),
+                                    "bytes_per_element": {"h2d": 12, "d2h": 14},
+                                    "published_peak_GBps_per_direction": HOST_LINK_PEAK_GBPS,
+                                    "published_peak_note": "PCIe 5.0 x16, 32 GT/s x 16 lanes",
+                                    "frac_of_published_both_directions":
+                                        round((h2d + d2h) / (2 * HOST_LINK_PEAK_GBPS), 4),
+                                    "probe": probe}}),
           flush=True)
 
 
@@ -700,7 +757,15 @@ def run_interference(args):
     fused calls' time window during which a GEMM was executing.  With
     --cu-split K the fused call runs on a stream masked to K CUs and the GEMM
     on a stream masked to the other CUs (K = 0: both streams unmasked).
-    torch.matmul is the vendor GEMM, the antagonist only."""
+    --shape lists the library's launch shapes to measure (DISDP_LAUNCH_SHAPE:
+    solo, shared).  After each concurrent run the fused steps are run again
+    alone from the same start state and must give the same bits; sampled
+    elements are checked against the oracle's steps.  torch.matmul is the
+    vendor GEMM, the antagonist only.  Per setting the kernels run in this
+    order (the `phases` field), so a kernel trace can be cut into them:
+    2 warm-up fused calls and GEMMs interleaved, the fused calls alone, the
+    GEMMs alone, the concurrent GEMMs and fused calls, the fused calls again
+    alone for the check."""
     import numpy as np
     import torch
     import paper_2409_00918_amd as dd
@@ -720,12 +785,19 @@ def run_interference(args):
     n_cu = torch.cuda.get_device_properties(0).multi_processor_count
     t_state = [0]
     med = lambda x: float(np.median(x)) if len(x) else None
+    snap = [torch.empty_like(dp) for _ in range(3)]
+    conc_out = [torch.empty_like(x) for x in (dp, dm, dv, d16)]
+    sample = np.unique(np.random.default_rng(4).integers(0, wl.n, 1 << 16)).astype(np.int64)
+    ix = torch.from_numpy(sample).cuda()
+    g_sample = [g[ix].cpu().numpy() for g in dg]
 
-    def fused(stream):
-        t_state[0] += 1
+    def fused(stream, t=None):
+        if t is None:
+            t_state[0] += 1
+            t = t_state[0]
         dd.aggregate_adam(dg, dp, dm, dv, d16, lr=hp["lr"], beta1=hp["beta1"],
                           beta2=hp["beta2"], eps=hp["eps"], weight_decay=hp["wd"],
-                          step=t_state[0], stream=stream)
+                          step=t, stream=stream)
 
     def gemm(stream):
         with torch.cuda.stream(stream):
@@ -745,59 +817,108 @@ def run_interference(args):
     def spans(origin, ev):
         return [(origin.elapsed_time(a), origin.elapsed_time(b)) for a, b in ev]
 
-    for k in [int(x) for x in args.cu_split.split(",")]:
-        handles = []
-        if k == 0:
-            side, comp = torch.cuda.Stream(), torch.cuda.Stream()
-        else:
-            side, h1, hip = _cu_mask_stream(0, k, n_cu)
-            comp, h2, _ = _cu_mask_stream(k, n_cu - k, n_cu)
-            handles = [(hip, h1), (hip, h2)]
-        for _ in range(2):
-            fused(side)
-            gemm(comp)
+    def check(side, t_first, reps):
+        """The concurrent result against the same steps run alone from the
+        snapshot, and sampled elements against the oracle."""
+        import oracle
+        for dst, src in zip(conc_out, (dp, dm, dv, d16)):
+            dst.copy_(src)
+        pre = [x[ix].cpu().numpy() for x in snap]
+        for dst, src in zip((dp, dm, dv), snap):
+            dst.copy_(src)
         torch.cuda.synchronize()
-        origin = torch.cuda.Event(enable_timing=True)
-        origin.record(torch.cuda.current_stream())
+        for k in range(reps):
+            fused(side, t_first + k)
         torch.cuda.synchronize()
-        ev = enqueue(side, fused, args.steps)
-        torch.cuda.synchronize()
-        f_solo = spans(origin, ev)
-        ev = enqueue(comp, gemm, 30)
-        torch.cuda.synchronize()
-        g_solo = spans(origin, ev)
-        fs_ms = med([e - b for b, e in f_solo])
-        gs_ms = med([e - b for b, e in g_solo])
-        n_gemm = int(3 * args.steps * fs_ms / gs_ms) + 10
-        evg = enqueue(comp, gemm, n_gemm)
-        evf = enqueue(side, fused, args.steps)
-        torch.cuda.synchronize()
-        g_conc, f_conc = spans(origin, evg), spans(origin, evf)
-        w0, w1 = min(b for b, _ in f_conc), max(e for _, e in f_conc)
-        inside = [e - b for b, e in g_conc if b >= w0 and e <= w1]
-        busy = sum(max(0.0, min(e, w1) - max(b, w0)) for b, e in g_conc) / (w1 - w0)
-        fc_ms = med([e - b for b, e in f_conc])
-        gc_ms = med(inside)
-        line = {
-            "metric": "interference: fused aggregate+AdamW vs a concurrent bf16 GEMM loop",
-            "workload": wl.name, "gemm": "bf16 8192x8192x8192 (torch.matmul)",
-            "cu_split": None if k == 0 else {"fused_cus": k, "gemm_cus": n_cu - k},
-            "fused_solo_ms": round(fs_ms, 4), "fused_concurrent_ms": round(fc_ms, 4),
-            "fused_slowdown": round(fc_ms / fs_ms, 3),
-            "fused_solo_TBps": round(wl.n * 58 / (fs_ms * 1e-3) / 1e12, 3),
-            "gemm_solo_ms": round(gs_ms, 4),
-            "gemm_concurrent_ms": None if gc_ms is None else round(gc_ms, 4),
-            "gemm_slowdown": None if gc_ms is None else round(gc_ms / gs_ms, 3),
-            "gemm_solo_tflops": round(2 * 8192**3 / (gs_ms * 1e-3) / 1e12, 1),
-            "gemms_inside_fused_window": len(inside),
-            "gemm_busy_frac": round(busy, 3),
-            "fused_reps": args.steps,
-            "streams": "default priority" + ("" if k == 0 else ", CU-masked"),
-        }
-        print(json.dumps(line), flush=True)
-        torch.cuda.synchronize()
-        for hip, h in handles:
-            hip.hipStreamDestroy(h)
+        same = all(torch.equal(a, b) for a, b in zip(conc_out, (dp, dm, dv, d16)))
+        p, m, v = pre
+        for k in range(reps):
+            want = oracle.fused(g_sample, p, m, v, t=t_first + k, **hp)
+            p, m, v = want["p"], want["m"], want["v"]
+        got = [x[ix].cpu().numpy() for x in conc_out]
+        ok = (np.array_equal(got[0].view(np.uint32), want["p"].view(np.uint32)) and
+              np.array_equal(got[1].view(np.uint32), want["m"].view(np.uint32)) and
+              np.array_equal(got[2].view(np.uint32), want["v"].view(np.uint32)) and
+              np.array_equal(got[3].view(np.uint16), want["p16"]))
+        return {"concurrent_equals_solo_all_elements": bool(same),
+                "oracle_sampled_elements": int(sample.size), "oracle_bit_exact": bool(ok)}
+
+    saved_shape = os.environ.get("DISDP_LAUNCH_SHAPE")
+    all_ok = True
+    for shape in args.shape.split(","):
+        os.environ["DISDP_LAUNCH_SHAPE"] = shape
+        for k in [int(x) for x in args.cu_split.split(",")]:
+            handles = []
+            if k == 0:
+                side, comp = torch.cuda.Stream(), torch.cuda.Stream()
+            else:
+                side, h1, hip = _cu_mask_stream(0, k, n_cu)
+                comp, h2, _ = _cu_mask_stream(k, n_cu - k, n_cu)
+                handles = [(hip, h1), (hip, h2)]
+            for _ in range(2):
+                fused(side)
+                gemm(comp)
+            torch.cuda.synchronize()
+            origin = torch.cuda.Event(enable_timing=True)
+            origin.record(torch.cuda.current_stream())
+            torch.cuda.synchronize()
+            ev = enqueue(side, fused, args.steps)
+            torch.cuda.synchronize()
+            f_solo = spans(origin, ev)
+            n_gemm_solo = 30
+            ev = enqueue(comp, gemm, n_gemm_solo)
+            torch.cuda.synchronize()
+            g_solo = spans(origin, ev)
+            fs_ms = med([e - b for b, e in f_solo])
+            gs_ms = med([e - b for b, e in g_solo])
+            n_gemm = int(3 * args.steps * fs_ms / gs_ms) + 10
+            for dst, src in zip(snap, (dp, dm, dv)):
+                dst.copy_(src)
+            torch.cuda.synchronize()
+            t_first = t_state[0] + 1
+            evg = enqueue(comp, gemm, n_gemm)
+            evf = enqueue(side, fused, args.steps)
+            torch.cuda.synchronize()
+            g_conc, f_conc = spans(origin, evg), spans(origin, evf)
+            w0, w1 = min(b for b, _ in f_conc), max(e for _, e in f_conc)
+            inside = [e - b for b, e in g_conc if b >= w0 and e <= w1]
+            busy = sum(max(0.0, min(e, w1) - max(b, w0)) for b, e in g_conc) / (w1 - w0)
+            fc_ms = med([e - b for b, e in f_conc])
+            gc_ms = med(inside)
+            parity = check(side, t_first, args.steps)
+            all_ok = all_ok and parity["concurrent_equals_solo_all_elements"] and \
+                parity["oracle_bit_exact"]
+            line = {
+                "metric": "interference: fused aggregate+AdamW vs a concurrent bf16 GEMM loop",
+                "workload": wl.name, "gemm": "bf16 8192x8192x8192 (torch.matmul)",
+                "launch_shape": shape,
+                "cu_split": None if k == 0 else {"fused_cus": k, "gemm_cus": n_cu - k},
+                "fused_solo_ms": round(fs_ms, 4), "fused_concurrent_ms": round(fc_ms, 4),
+                "fused_slowdown": round(fc_ms / fs_ms, 3),
+                "fused_solo_TBps": round(wl.n * 58 / (fs_ms * 1e-3) / 1e12, 3),
+                "gemm_solo_ms": round(gs_ms, 4),
+                "gemm_concurrent_ms": None if gc_ms is None else round(gc_ms, 4),
+                "gemm_slowdown": None if gc_ms is None else round(gc_ms / gs_ms, 3),
+                "gemm_solo_tflops": round(2 * 8192**3 / (gs_ms * 1e-3) / 1e12, 1),
+                "gemms_inside_fused_window": len(inside),
+                "gemm_busy_frac": round(busy, 3),
+                "fused_reps": args.steps,
+                "phases": {"warmup_fused_and_gemm": 2, "fused_solo": args.steps,
+                           "gemm_solo": n_gemm_solo, "gemm_concurrent": n_gemm,
+                           "fused_concurrent": args.steps, "fused_check": args.steps},
+                "parity": parity,
+                "streams": "default priority" + ("" if k == 0 else ", CU-masked"),
+            }
+            print(json.dumps(line), flush=True)
+            torch.cuda.synchronize()
+            for hip, h in handles:
+                hip.hipStreamDestroy(h)
+    if saved_shape is None:
+        os.environ.pop("DISDP_LAUNCH_SHAPE", None)
+    else:
+        os.environ["DISDP_LAUNCH_SHAPE"] = saved_shape
+    if not all_ok:
+        raise SystemExit("interference: a concurrent result differs from the solo run")
 
 
 def run_copy_probe(args):
@@ -842,6 +963,8 @@ def main(argv=None):
     ap.add_argument("--interference", action="store_true")
     ap.add_argument("--cu-split", default="0,32,64,128",
                     help="interference: CUs given to the fused call (0 = shared)")
+    ap.add_argument("--shape", default="solo,shared",
+                    help="interference: the library's launch shapes to measure")
     ap.add_argument("--copy-probe", action="store_true")
     ap.add_argument("--quantize", action="store_true",
                     help="time the format conversion over the shard's contributions")

@@ -15,7 +15,8 @@ What it computes (arXiv 2409.00918):
   * ``quantize_array``  -- that format conversion over a buffer.
   * ``adamw``           -- the parameter server's mixed-precision Adam step,
                           step 5 of the backward stage (Section III-D, Table III).
-  * ``fused``           -- the two composed, element by element.
+  * ``fused``           -- the two composed, element by element
+                          (``fused_inplace``: the same on caller arrays).
   * ``bf16_rne``        -- the 2-byte parameter copy written by step 5.
 
 All floating-point work happens in the C file in IEEE binary32 with the
@@ -258,6 +259,24 @@ def fused(gs: Sequence[np.ndarray], p, m, v, *, mode=AGG_FP32, frac_bits=0,
     if want_agg_i32:
         out["agg_i32"] = ai
     return out
+
+
+def fused_inplace(gs: Sequence[np.ndarray], p: np.ndarray, m: np.ndarray, v: np.ndarray,
+                  p16: Optional[np.ndarray], *, mode=AGG_FP32, frac_bits=0, lr, beta1,
+                  beta2, eps, wd, t, grad_scale=1.0) -> None:
+    """The same step as ``fused`` on caller-owned arrays, updated in place:
+    p, m, v float32 and p16 uint16 (or None), all contiguous, nothing
+    allocated or copied -- for timing the oracle itself."""
+    n = _check_n(gs)
+    for a in (p, m, v) + (() if p16 is None else (p16,)):
+        if a.size != n or not a.flags.c_contiguous:
+            raise ValueError("state arrays must be contiguous and of the shard's length")
+    if p.dtype != np.float32 or m.dtype != np.float32 or v.dtype != np.float32 or \
+            (p16 is not None and p16.dtype != np.uint16):
+        raise TypeError("p, m, v must be float32 and p16 uint16")
+    lib().oracle_fused(_ptr_array(gs), len(gs), _grad_dtype(gs), n, mode, frac_bits,
+                       p.ctypes.data, m.ctypes.data, v.ctypes.data, _ptr(p16), None, None,
+                       lr, beta1, beta2, eps, wd, t, grad_scale)
 
 
 def fp_env_ok() -> bool:

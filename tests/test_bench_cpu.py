@@ -83,7 +83,8 @@ def test_cpu_baseline_leg_on_a_tiny_sample(monkeypatch):
     p, m, v = (torch.from_numpy(x) for x in synth.host_state(wl.wid, n))
     r = bench.cpu_baseline(wl, gs, p, m, v)
     assert r["kind"] == "oracle" and r["cores"] == 1 and r["unit"] == "G params/s"
-    assert r["value"] > 0 and "2048 elements" in r["sample"]
+    assert r["value"] > 0 and "first 2,048 of" in r["sample"]
+    assert r["sample_fraction"] == round(2048 / wl.n, 4)
     # the sample is read, not modified
     assert np.array_equal(p.numpy(), synth.host_state(wl.wid, n)[0])
 
@@ -99,13 +100,13 @@ def test_cpu_baseline_threads_cover_the_sample_like_one_call(monkeypatch):
     monkeypatch.setattr(bench, "CPU_STEPS", 2)
     calls = []
     real = oracle.fused
+    real_inplace = oracle.fused_inplace
 
-    def spy(gs, p, m, v, **kw):
-        out = real(gs, p, m, v, **kw)
-        calls.append((kw["t"], p.size, out["p"]))
-        return out
+    def spy(gs, p, m, v, p16, **kw):
+        real_inplace(gs, p, m, v, p16, **kw)
+        calls.append((kw["t"], p.size, p.copy()))
 
-    monkeypatch.setattr(oracle, "fused", spy)
+    monkeypatch.setattr(oracle, "fused_inplace", spy)
     gs = [torch.from_numpy(g) for g in synth.host_grads(wl.wid, 1, wl.W, n, wl.sigma)]
     p, m, v = (torch.from_numpy(x) for x in synth.host_state(wl.wid, n))
     r = bench.cpu_baseline(wl, gs, p, m, v, threads=3)

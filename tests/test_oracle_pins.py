@@ -623,3 +623,18 @@ def test_quantise_then_aggregate_equals_aggregate_of_floats(gdtype):
     y = oracle.fused(qs, p, m, v, mode=oracle.AGG_FIXED, frac_bits=k, t=2, **HP)
     for key in ("p", "m", "v", "p16"):
         assert np.array_equal(x[key], y[key])
+
+
+def test_fused_inplace_equals_fused():
+    """The in-place wrapper (used to time the oracle) runs the same C step."""
+    gs = synth.host_grads(77, 2, 4, 5003, 1e-4, outlier_frac=0.01, outlier_scale=100.0)
+    p, m, v = synth.host_state(77, 5003, mv_sigma=1e-4)
+    hp = dict(lr=np.float32(1e-4), beta1=np.float32(0.9), beta2=np.float32(0.95),
+              eps=np.float32(1e-8), wd=np.float32(0.1))
+    for mode in (oracle.AGG_FP32, oracle.AGG_FIXED):
+        want = oracle.fused(gs, p, m, v, mode=mode, frac_bits=24, t=2, **hp)
+        q, mm, vv = p.copy(), m.copy(), v.copy()
+        q16 = np.zeros(p.size, np.uint16)
+        oracle.fused_inplace(gs, q, mm, vv, q16, mode=mode, frac_bits=24, t=2, **hp)
+        for k, a in (("p", q), ("m", mm), ("v", vv), ("p16", q16)):
+            assert np.array_equal(a.view(a.dtype), want[k]), k
