@@ -85,7 +85,7 @@ def probe_lib():
 def committed_traffic(workload: str, src_hash: str):
     """HBM bytes per launch from the committed counter summary of this
     workload, if it was taken on the current kernel source."""
-    path = os.path.join(ROOT, "profiles", f"counters_fused_{workload}.md")
+    path = os.path.join(ROOT, "profiles", f"fused_{workload}.md")
     if not os.path.exists(path):
         return None
     with open(path) as f:

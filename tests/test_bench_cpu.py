@@ -31,7 +31,7 @@ def test_kernel_source_hash_is_stable():
 def _records():
     out = []
     for name in sorted(os.listdir(os.path.join(ROOT, "profiles"))):
-        if not name.startswith("counters_fused_"):
+        if not name.startswith("fused_"):
             continue
         with open(os.path.join(ROOT, "profiles", name)) as f:
             for line in f:
@@ -50,7 +50,7 @@ def test_committed_counter_records_are_consistent():
     assert recs, "no counter summaries under profiles/"
     for name, r in recs:
         wl = synth.WORKLOADS[r["workload"]]
-        assert name == f"counters_fused_{wl.name}.md"
+        assert name == f"fused_{wl.name}.md"
         # each of the three is rounded to whole bytes on its own
         assert abs(r["read_bytes_per_launch"] + r["write_bytes_per_launch"]
                    - r["bytes_per_launch"]) <= 2
@@ -63,6 +63,31 @@ def test_committed_counter_records_are_consistent():
             pytest.approx(r["read_bytes_per_launch"], rel=1e-4)
         assert r["write_kib_per_dispatch"] * 1024 * r["write_scale"] == \
             pytest.approx(r["write_bytes_per_launch"], rel=1e-4)
+
+
+def test_committed_bench_lines_reproduce_their_roofline():
+    """The bench line committed in each fused-kernel summary: achieved =
+    N x algorithmic bytes per element / the average kernel time, frac =
+    achieved / 8 TB/s, and the G params/s value = N / wall time per step."""
+    import paper_2409_00918_amd as dd
+    found = 0
+    for name in sorted(os.listdir(os.path.join(ROOT, "profiles"))):
+        if not name.startswith("fused_"):
+            continue
+        with open(os.path.join(ROOT, "profiles", name)) as f:
+            lines = [json.loads(x) for x in f if x.startswith('{"metric"')]
+        for d in lines:
+            found += 1
+            wl = synth.WORKLOADS[d["config"]["workload"]]
+            r = d["roofline"]
+            bpe = dd.algorithmic_bytes_per_element(wl.W, 2 if wl.gdtype == "bf16" else 4)
+            assert r["algorithmic_bytes_per_element"] == bpe
+            assert r["achieved"] == pytest.approx(wl.n * bpe / (r["avg_kernel_ms"] * 1e-3) / 1e9,
+                                                  rel=2e-4)
+            assert r["frac"] == pytest.approx(r["achieved"] / r["peak"], abs=1e-4)
+            assert d["value"] == pytest.approx(wl.n / (d["ms_per_step"] * 1e-3) / 1e9, rel=2e-4)
+            assert d["config"]["n"] == wl.n and d["config"]["W"] == wl.W
+    assert found >= 3
 
 
 def test_committed_traffic_is_tied_to_the_kernel_source():
