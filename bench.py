@@ -756,7 +756,9 @@ def run_interference(args):
     overlap is observed, not assumed: `gemm_busy_frac` is the share of the
     fused calls' time window during which a GEMM was executing.  With
     --cu-split K the fused call runs on a stream masked to K CUs and the GEMM
-    on a stream masked to the other CUs (K = 0: both streams unmasked).
+    on a stream masked to the other CUs (K = 0: both streams on every CU;
+    they are still created with a full CU mask, which gives each its own
+    hardware queue).
     --shape lists the library's launch shapes to measure (DISDP_LAUNCH_SHAPE:
     solo, shared).  After each concurrent run the fused steps are run again
     alone from the same start state and must give the same bits; sampled
@@ -848,13 +850,16 @@ def run_interference(args):
     for shape in args.shape.split(","):
         os.environ["DISDP_LAUNCH_SHAPE"] = shape
         for k in [int(x) for x in args.cu_split.split(",")]:
-            handles = []
             if k == 0:
-                side, comp = torch.cuda.Stream(), torch.cuda.Stream()
+                # both streams on every CU: a CU-masked stream has a hardware
+                # queue of its own, whereas two ordinary streams can share
+                # one and then run one after the other
+                side, h1, hip = _cu_mask_stream(0, n_cu, n_cu)
+                comp, h2, _ = _cu_mask_stream(0, n_cu, n_cu)
             else:
                 side, h1, hip = _cu_mask_stream(0, k, n_cu)
                 comp, h2, _ = _cu_mask_stream(k, n_cu - k, n_cu)
-                handles = [(hip, h1), (hip, h2)]
+            handles = [(hip, h1), (hip, h2)]
             for _ in range(2):
                 fused(side)
                 gemm(comp)
@@ -907,7 +912,7 @@ def run_interference(args):
                            "gemm_solo": n_gemm_solo, "gemm_concurrent": n_gemm,
                            "fused_concurrent": args.steps, "fused_check": args.steps},
                 "parity": parity,
-                "streams": "default priority" + ("" if k == 0 else ", CU-masked"),
+                "streams": "default priority, CU-masked" + (" (full mask: every CU)" if k == 0 else ""),
             }
             print(json.dumps(line), flush=True)
             torch.cuda.synchronize()

@@ -14,6 +14,22 @@ import oracle
 import synth
 from gpu_common import HP, assert_parity, run_fused_case, to_dev, to_host, torch
 
+
+def _cu_masked_stream(n_cus):
+    """A default-priority stream on the first n_cus CUs
+    (hipExtStreamCreateWithCUMask on torch's HIP runtime)."""
+    import ctypes
+    t_ = torch()
+    total = t_.cuda.get_device_properties(0).multi_processor_count
+    hip = ctypes.CDLL("libamdhip64.so.7")          # torch's runtime, already loaded
+    words = (total + 31) // 32
+    mask = (ctypes.c_uint32 * words)()
+    for cu in range(min(n_cus, total)):
+        mask[cu // 32] |= 1 << (cu % 32)
+    h = ctypes.c_void_p()
+    assert hip.hipExtStreamCreateWithCUMask(ctypes.byref(h), ctypes.c_uint32(words), mask) == 0
+    return t_.cuda.ExternalStream(h.value), h, hip
+
 pytestmark = pytest.mark.gpu
 
 SHAPES = ["solo", "shared"]
@@ -113,21 +129,44 @@ def test_fused_next_to_a_gemm_loop_equals_solo(shape, mode):
     kw = dict(lr=HP["lr"], beta1=HP["beta1"], beta2=HP["beta2"], eps=HP["eps"],
               weight_decay=HP["wd"], mode=mode, frac_bits=24)
 
+    # streams with a full CU mask: each has a hardware queue of its own, so
+    # the GEMMs and the fused steps really run at the same time
+    total = t_.cuda.get_device_properties(0).multi_processor_count
+    (side, hs, hip), (comp, hc, _) = _cu_masked_stream(total), _cu_masked_stream(total)
+
     def run(concurrent):
         st = [x.clone() for x in (p0, m0, v0)] + [t_.empty(n, dtype=t_.int16, device="cuda")]
-        side, comp = t_.cuda.Stream(), t_.cuda.Stream()
         t_.cuda.synchronize()
+        ev = []
         if concurrent:
             with t_.cuda.stream(comp):
                 for _ in range(60):
+                    a, b = t_.cuda.Event(enable_timing=True), t_.cuda.Event(enable_timing=True)
+                    a.record(comp)
                     t_.matmul(A, B, out=C)
+                    b.record(comp)
+                    ev.append((a, b))
+        f0, f1 = t_.cuda.Event(enable_timing=True), t_.cuda.Event(enable_timing=True)
+        f0.record(side)
         for t in range(1, K + 1):
             dd.aggregate_adam(dg, *st, step=t, stream=side, **kw)
+        f1.record(side)
         t_.cuda.synchronize()
-        return st
+        # GEMMs that started before the fused steps ended and ended after
+        # they started: the two overlapped
+        overlap = sum(1 for a, b in ev
+                      if f0.elapsed_time(b) > 0 and a.elapsed_time(f1) > 0)
+        return st, overlap
 
-    solo = run(False)
-    conc = run(True)
+    try:
+        solo, _ = run(False)
+        conc, overlap = run(True)
+    finally:
+        t_.cuda.synchronize()
+        hip.hipStreamDestroy(hs)
+        hip.hipStreamDestroy(hc)
+    print(f"[shapes] {shape} {mode}: {overlap} GEMMs overlapped the fused steps", flush=True)
+    assert overlap > 0, "the GEMM loop and the fused steps did not overlap"
     for name, a, b in zip(("p", "m", "v", "p16"), solo, conc):
         assert t_.equal(a, b), f"{shape} {mode}: {name} differs next to the GEMM"
     idx = np.unique(np.concatenate([np.random.default_rng(8).integers(0, n, 1 << 15),
