@@ -336,3 +336,38 @@ def test_state_in_pinned_host_memory_at_scale():
     finally:
         del dg, host, h16, snap
         t_.cuda.empty_cache()
+
+
+def test_full_size_shard_in_the_shared_launch_shape(monkeypatch):
+    """The 7B/8 shard in the four-wave launch shape (DISDP_LAUNCH_SHAPE=
+    shared, the shape for a GPU shared with compute kernels): every element
+    of t = 1 against the oracle."""
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    wl = synth.WORKLOADS["opt7b_shard8_w8_f32"]
+    free = room_for(wl)
+    if bytes_needed(wl) > 0.92 * free:
+        pytest.skip("not enough device memory")
+    monkeypatch.setenv("DISDP_LAUNCH_SHAPE", "shared")
+    n, W = wl.n, wl.W
+    sh = dd.allocate_shard(n, W, wl.gdtype)
+    synth.device_grads(wl.wid, 1, W, n, wl.sigma, outlier_frac=wl.outlier_frac,
+                       outlier_scale=wl.outlier_scale, out=sh.grads)
+    synth.device_state(wl.wid, n, wl.p_sigma, out=(sh.param, sh.m, sh.v))
+    snap = [x.clone() for x in (sh.param, sh.m, sh.v)]
+    hp = dict(lr=np.float32(wl.lr), beta1=np.float32(wl.beta1), beta2=np.float32(wl.beta2),
+              eps=np.float32(wl.eps), wd=np.float32(wl.wd))
+    try:
+        dd.aggregate_adam(sh.grads, sh.param, sh.m, sh.v, sh.param_bf16, lr=hp["lr"],
+                          beta1=hp["beta1"], beta2=hp["beta2"], eps=hp["eps"],
+                          weight_decay=hp["wd"], step=1)
+        t_.cuda.synchronize()
+        bad = whole_shard_mismatches(sh.grads, snap, {"p": sh.param, "m": sh.m, "v": sh.v,
+                                                      "p16": sh.param_bf16},
+                                     gdtype="f32", mode="fp32", frac_bits=0, t=1, hp=hp,
+                                     label="shared shape step 1")
+        assert bad["elements"] == n
+        assert all(c == 0 for k, c in bad.items() if k != "elements"), bad
+    finally:
+        del sh, snap
+        t_.cuda.empty_cache()
