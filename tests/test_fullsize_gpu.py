@@ -371,3 +371,59 @@ def test_full_size_shard_in_the_shared_launch_shape(monkeypatch):
     finally:
         del sh, snap
         t_.cuda.empty_cache()
+
+
+def test_full_size_int32_contributions_equal_the_float_path():
+    """NEXT-1 at full size: W = 8 contributions of the 7B/8 recipe converted
+    by disdp_quantize to the switch's int32 format at 2^24 and summed as
+    DISDP_DT_I32, against the same fp32 contributions converted inside the
+    fused kernel (fixed mode; that path is checked element by element
+    against the oracle on the 175B/64 shard).  t = 1 and t = 2 from the same
+    state: every element of p, m, v, the bf16 copy and the int32 aggregate
+    must be equal, compared on the device; sampled elements of the quantized
+    contributions against the oracle's conversion."""
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    wl = synth.WORKLOADS["opt7b_shard8_w8_f32"]
+    n, W, k = wl.n, wl.W, 24
+    free, _ = t_.cuda.mem_get_info()
+    need = n * (W * 8 + 2 * (12 + 2 + 4))
+    if need > 0.9 * free:
+        pytest.skip("not enough device memory")
+    print(f"[fullsize] int32 contributions n={n}", flush=True)
+    gf = synth.device_grads(wl.wid, 1, W, n, wl.sigma, outlier_frac=wl.outlier_frac,
+                            outlier_scale=wl.outlier_scale)
+    gi = [t_.empty(n, dtype=t_.int32, device="cuda") for _ in range(W)]
+    idx = sample_indices(n, 41)
+    ix = t_.from_numpy(idx).cuda()
+    hp = dict(lr=np.float32(wl.lr), beta1=np.float32(wl.beta1), beta2=np.float32(wl.beta2),
+              eps=np.float32(wl.eps), wd=np.float32(wl.wd))
+    kw = dict(lr=hp["lr"], beta1=hp["beta1"], beta2=hp["beta2"], eps=hp["eps"],
+              weight_decay=hp["wd"], mode="fixed", frac_bits=k)
+    a = list(synth.device_state(wl.wid, n, wl.p_sigma))
+    b = [x.clone() for x in a]
+    a16, b16 = (t_.empty(n, dtype=t_.int16, device="cuda") for _ in range(2))
+    ai, bi = (t_.empty(n, dtype=t_.int32, device="cuda") for _ in range(2))
+    try:
+        for t in (1, 2):
+            if t > 1:
+                synth.device_grads(wl.wid, t, W, n, wl.sigma, outlier_frac=wl.outlier_frac,
+                                   outlier_scale=wl.outlier_scale, out=gf)
+            for w in range(W):
+                dd.quantize(gf[w], gi[w], frac_bits=k)
+            t_.cuda.synchronize()
+            for w in range(W):
+                want = oracle.quantize_array(to_host(gf[w][ix]), k)
+                assert np.array_equal(to_host(gi[w][ix]), want), f"quantize w={w} t={t}"
+            dd.aggregate_adam(gf, *a, a16, step=t, agg_out_i32=ai, **kw)
+            dd.aggregate_adam(gi, *b, b16, step=t, agg_out_i32=bi, **kw)
+            t_.cuda.synchronize()
+            for name, x, y in (("p", a[0], b[0]), ("m", a[1], b[1]), ("v", a[2], b[2]),
+                               ("p16", a16, b16), ("agg_i32", ai, bi)):
+                assert t_.equal(x.view(t_.int32) if x.dtype == t_.float32 else x,
+                                y.view(t_.int32) if y.dtype == t_.float32 else y), \
+                    f"t={t}: {name} differs between int32 and float contributions"
+            print(f"[fullsize] int32 contributions step {t} ok (all {n} elements)", flush=True)
+    finally:
+        del gf, gi, a, b, a16, b16, ai, bi
+        t_.cuda.empty_cache()
