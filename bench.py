@@ -105,14 +105,36 @@ def hparams(wl):
                 wd=np.float32(wl.wd))
 
 
+CONTIGUOUS = True   # --allocator: one physically contiguous block, or torch's allocator
+
+
+def workload(args):
+    """The workload named by --workload, with --n / --W overrides (for
+    sweeps; the name then records them)."""
+    import dataclasses
+    import synth
+    wl = synth.WORKLOADS[args.workload]
+    n = getattr(args, "n", None)
+    W = getattr(args, "W", None)
+    if n or W:
+        wl = dataclasses.replace(wl, n=n or wl.n, W=W or wl.W,
+                                 name=f"{wl.name}@n={n or wl.n},W={W or wl.W}")
+    return wl
+
+
+def shard(n, W, gdtype, **kw):
+    """dd.allocate_shard with the process's allocator choice."""
+    import paper_2409_00918_amd as dd
+    return dd.allocate_shard(n, W, gdtype, contiguous=CONTIGUOUS, **kw)
+
+
 def allocate(wl):
     """The shard's arrays in one allocation placed by disdp_shard_layout
     (as a parameter server would lay out its shard), filled with the seeded
     step-1 inputs.  The returned Shard owns the allocation; its fields are
     views into it."""
-    import paper_2409_00918_amd as dd
     import synth
-    sh = dd.allocate_shard(wl.n, wl.W, wl.gdtype)
+    sh = shard(wl.n, wl.W, wl.gdtype)
     synth.device_grads(wl.wid, 1, wl.W, wl.n, wl.sigma, gdtype=wl.gdtype,
                        outlier_frac=wl.outlier_frac, outlier_scale=wl.outlier_scale,
                        out=sh.grads)
@@ -231,7 +253,7 @@ def run_bench(args):
     import paper_2409_00918_amd as dd
     import synth
 
-    wl = synth.WORKLOADS[args.workload]
+    wl = workload(args)
     torch.cuda.set_device(0)
     dd.lib()
     hp = hparams(wl)
@@ -242,7 +264,7 @@ def run_bench(args):
         # fused call sums int32 contributions (fixed mode at the shard's scale)
         if wl.mode != "fixed":
             raise SystemExit("--contributions i32 needs a fixed-point workload")
-        sh = dd.allocate_shard(wl.n, wl.W, "i32")
+        sh = shard(wl.n, wl.W, "i32")
         for w in range(wl.W):
             g = synth.device_grad(wl.wid, 1, w, wl.n, wl.sigma, wl.gdtype,
                                   wl.outlier_frac, wl.outlier_scale)
@@ -400,7 +422,7 @@ def run_host_state(args):
     import torch
     import paper_2409_00918_amd as dd
     import synth
-    wl = synth.WORKLOADS[args.workload]
+    wl = workload(args)
     torch.cuda.set_device(0)
     dd.lib()
     probe = host_link_probe()
@@ -464,7 +486,7 @@ def run_quantize(args):
     import torch
     import paper_2409_00918_amd as dd
     import synth
-    wl = synth.WORKLOADS[args.workload]
+    wl = workload(args)
     torch.cuda.set_device(0)
     dd.lib()
     dg = synth.device_grads(wl.wid, 1, wl.W, wl.n, wl.sigma, gdtype=wl.gdtype,
@@ -515,7 +537,7 @@ def run_entry(args):
     import torch
     import paper_2409_00918_amd as dd
     import synth
-    wl = synth.WORKLOADS[args.workload]
+    wl = workload(args)
     torch.cuda.set_device(0)
     dd.lib()
     hp = hparams(wl)
@@ -552,7 +574,7 @@ def run_entry(args):
         def call(t):
             graph.replay()
     elif args.entry == "adam_step":
-        sh = dd.allocate_shard(wl.n, 1, "f32")
+        sh = shard(wl.n, 1, "f32")
         # an aggregate-sized gradient: one draw at sqrt(W) times the spread
         synth.device_grads(wl.wid, 1, 1, wl.n, wl.sigma * wl.W ** 0.5, out=sh.grads)
         agg = sh.grads[0]
@@ -562,7 +584,7 @@ def run_entry(args):
             dd.adam_step(agg, sh.param, sh.m, sh.v, sh.param_bf16, step=t, **kw)
     else:
         two = args.entry == "two_call"
-        sh = dd.allocate_shard(wl.n, wl.W, wl.gdtype, bf16_copy=two,
+        sh = shard(wl.n, wl.W, wl.gdtype, bf16_copy=two,
                                agg_f32=two or not fixed, agg_i32=fixed and not two)
         synth.device_grads(wl.wid, 1, wl.W, wl.n, wl.sigma, gdtype=wl.gdtype,
                            outlier_frac=wl.outlier_frac, outlier_scale=wl.outlier_scale,
@@ -963,6 +985,13 @@ def main(argv=None):
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--n", type=int, default=None,
+                    help="sweeps: override the workload's element count")
+    ap.add_argument("--W", type=int, default=None,
+                    help="sweeps: override the workload's contribution count")
+    ap.add_argument("--allocator", choices=["contiguous", "caching"], default="contiguous",
+                    help="shard slab: one physically contiguous block, or torch's "
+                         "caching allocator")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-copy-ceiling", action="store_true")
     ap.add_argument("--interference", action="store_true")
@@ -982,6 +1011,8 @@ def main(argv=None):
                     default="fused",
                     help="time another entry point on the same shard (not the headline)")
     args = ap.parse_args(argv)
+    global CONTIGUOUS
+    CONTIGUOUS = args.allocator == "contiguous"
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus > 1 or world > 1:
         print("bench.py measures one GPU: the shard's reduction and optimizer step "

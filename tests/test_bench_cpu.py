@@ -151,3 +151,17 @@ def test_cpu_baseline_threads_cover_the_sample_like_one_call(monkeypatch):
     want = [ref["p"][lo:hi] for lo, hi in zip(cuts[:-1], cuts[1:])]
     for w in want:
         assert any(g.size == w.size and np.array_equal(g, w) for g in got)
+
+
+def test_workload_overrides_for_sweeps():
+    """--n / --W give a renamed variant of the workload (so no committed
+    counter record of the real workload is attached to it); without them
+    the workload is the named one itself."""
+    import argparse
+    base = bench.workload(argparse.Namespace(workload="opt7b_shard8_w8_f32", n=None, W=None))
+    assert base is synth.WORKLOADS["opt7b_shard8_w8_f32"]
+    v = bench.workload(argparse.Namespace(workload="opt13b_shard16_w16_bf16", n=200_000_000,
+                                          W=24))
+    assert (v.n, v.W, v.gdtype, v.mode) == (200_000_000, 24, "bf16", "fp32")
+    assert v.name != base.name and v.name not in synth.WORKLOADS
+    assert bench.committed_traffic(v.name, bench.kernel_source_hash()) is None
