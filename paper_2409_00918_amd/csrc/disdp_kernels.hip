@@ -571,15 +571,26 @@ constexpr int fp32_mode_waves(int lane_bytes)
 // pieces (14).  Measured for fp32 W = 9, 24, 64 and bf16 W = 13, 32, 64.
 // Converting bf16 in fixed mode wants two more waves.  Fixed mode at
 // n = 4e8 over caps of 6-14 (TB/s at the chosen cap, the next best in
-// brackets): fp32 W = 9, 13, 20 10: 6.55, 6.47, 6.33 (12: 6.51; 8: 6.44,
-// 6.32); W = 24 8: 6.21 (6: 6.25); bf16 W = 17, 40 12: 6.35, 6.17 (14:
-// 6.24, 6.06); W = 32 10: 6.05 (12: 5.97).
+// brackets): fp32 W = 9, 13 10: 6.55, 6.47 (12: 6.51; 8: 6.44); bf16
+// W = 17, 40 12: 6.35, 6.17 (14: 6.24, 6.06); W = 32 10: 6.05 (12: 5.97).
+// Four-byte contributions (fp32 or int32) over two or more chunks keep
+// more round trips in flight per wave and want fewer waves: interleaved
+// at n = 2e8 over caps of 5-12, fp32 mode W = 17-32 6 waves (+0.4% to
+// +2.9% against 8-10), W = 40-64 5 waves (+3.0% to +4.8%); fixed mode
+// converting fp32, W = 17 7 waves (+1.6%), W = 20-64 6 waves (+0.2% to
+// +2.0%).  bf16 contributions were within about 1% of the best at the
+// rules above.
 int runtime_w_waves(int W, int gt, int mode)
 {
     const bool bf16 = gt == kGradBF16;
     const int chunk = bf16 ? 16 : 8;
-    if (mode == kAggFixed && gt != kGradI32)
+    if (mode == kAggFixed && gt != kGradI32) {
+        if (!bf16 && W >= 2 * chunk)
+            return W < 20 ? 7 : 6;
         return (W % chunk ? 10 : 8) + (bf16 ? 2 : 0);
+    }
+    if (!bf16 && W >= 2 * chunk)
+        return W <= 32 ? 6 : 5;
     return W < chunk ? 14 : W % chunk ? 10 : 8;
 }
 
