@@ -78,15 +78,21 @@ def test_committed_bench_lines_reproduce_their_roofline():
             lines = [json.loads(x) for x in f if x.startswith('{"metric"')]
         for d in lines:
             found += 1
-            wl = synth.WORKLOADS[d["config"]["workload"]]
+            # a sweep line names its workload with its overrides: name@n=..,W=..
+            name, _, over = d["config"]["workload"].partition("@")
+            wl = synth.WORKLOADS[name]
+            n, W = d["config"]["n"], d["config"]["W"]
+            if not over:
+                assert (n, W) == (wl.n, wl.W)
+            else:
+                assert over == f"n={n},W={W}"
             r = d["roofline"]
-            bpe = dd.algorithmic_bytes_per_element(wl.W, 2 if wl.gdtype == "bf16" else 4)
+            bpe = dd.algorithmic_bytes_per_element(W, 2 if wl.gdtype == "bf16" else 4)
             assert r["algorithmic_bytes_per_element"] == bpe
-            assert r["achieved"] == pytest.approx(wl.n * bpe / (r["avg_kernel_ms"] * 1e-3) / 1e9,
+            assert r["achieved"] == pytest.approx(n * bpe / (r["avg_kernel_ms"] * 1e-3) / 1e9,
                                                   rel=2e-4)
             assert r["frac"] == pytest.approx(r["achieved"] / r["peak"], abs=1e-4)
-            assert d["value"] == pytest.approx(wl.n / (d["ms_per_step"] * 1e-3) / 1e9, rel=2e-4)
-            assert d["config"]["n"] == wl.n and d["config"]["W"] == wl.W
+            assert d["value"] == pytest.approx(n / (d["ms_per_step"] * 1e-3) / 1e9, rel=2e-4)
     assert found >= 3
 
 
