@@ -529,6 +529,7 @@ def _hip_runtime() -> ctypes.CDLL:
         L.hipExtMallocWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_size_t,
                                             ctypes.c_uint]
         L.hipGetLastError.restype = ctypes.c_int
+        L.hipPeekAtLastError.restype = ctypes.c_int
         _hip = L
     return _hip
 
@@ -547,11 +548,13 @@ class _ContiguousBlock:
         hip = _hip_runtime()
         ptr = ctypes.c_void_p()
         with torch.cuda.device(device_index):
+            pending = hip.hipPeekAtLastError()
             rc = hip.hipExtMallocWithFlags(ctypes.byref(ptr), nbytes,
                                            _HIP_DEVICE_MALLOC_CONTIGUOUS)
         self.ptr = ptr.value or 0
         if rc != 0 or not self.ptr:
-            hip.hipGetLastError()           # clear the recorded error
+            if pending == 0:                # clear the error this call recorded,
+                hip.hipGetLastError()       # never one that was already pending
             raise MemoryError(f"no physically contiguous block of {nbytes} bytes "
                               f"(HIP error {rc})")
         self.nbytes = nbytes
