@@ -655,6 +655,16 @@ int main(int argc, char **argv)
     fused_case("fp32 W=3 pinned host state", 3, DISDP_DT_F32, 300007, DISDP_AGG_FP32, 0, 2, true,
                false);
     std::fflush(stdout);
+    // the launch shape for a GPU shared with compute kernels, chosen through
+    // the environment on each call: same results, checked against the oracle
+    setenv("DISDP_LAUNCH_SHAPE", "shared", 1);
+    fused_case("shared shape fp32 W=8 device state", 8, DISDP_DT_F32, 1000003, DISDP_AGG_FP32,
+               0, 2, false, true);
+    std::fflush(stdout);
+    fused_case("shared shape fixed W=24 device state", 24, DISDP_DT_F32, 300007,
+               DISDP_AGG_FIXED, 24, 2, false, true);
+    std::fflush(stdout);
+    unsetenv("DISDP_LAUNCH_SHAPE");
     graph_case("graph replay fp32 W=6", 6, DISDP_DT_F32, 500009, DISDP_AGG_FP32, 0, 4);
     std::fflush(stdout);
     graph_case("graph replay fixed bf16 W=13", 13, DISDP_DT_BF16, 200003, DISDP_AGG_FIXED, 24, 3);

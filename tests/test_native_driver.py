@@ -1,7 +1,8 @@
 """The C ABI from a plain C++ program (tests/native/abi_driver.cpp): no
 PyTorch, the system HIP runtime, hipMalloc / hipHostMalloc buffers, a
 created stream, the error codes a C caller sees, and bit parity with the
-CPU oracle for the fused call in both modes, the int32-contribution path,
+CPU oracle for the fused call in both modes and in both launch shapes
+(DISDP_LAUNCH_SHAPE set from C), the int32-contribution path,
 a slab placed by disdp_shard_layout, and a shard in memory from the
 virtual-memory API (hipMemCreate / hipMemMap, as VMM-based allocators hand
 it out)."""
