@@ -783,8 +783,8 @@ def run_interference(args):
     hardware queue).
     --shape lists the library's launch shapes to measure (DISDP_LAUNCH_SHAPE:
     solo, shared).  After each concurrent run the fused steps are run again
-    alone from the same start state and must give the same bits; sampled
-    elements are checked against the oracle's steps.  torch.matmul is the
+    alone from the same start state and must give the same bits on every
+    element.  torch.matmul is the
     vendor GEMM, the antagonist only.  Per setting the kernels run in this
     order (the `phases` field), so a kernel trace can be cut into them:
     2 warm-up fused calls and GEMMs interleaved, the fused calls alone, the
@@ -811,9 +811,6 @@ def run_interference(args):
     med = lambda x: float(np.median(x)) if len(x) else None
     snap = [torch.empty_like(dp) for _ in range(3)]
     conc_out = [torch.empty_like(x) for x in (dp, dm, dv, d16)]
-    sample = np.unique(np.random.default_rng(4).integers(0, wl.n, 1 << 16)).astype(np.int64)
-    ix = torch.from_numpy(sample).cuda()
-    g_sample = [g[ix].cpu().numpy() for g in dg]
 
     def fused(stream, t=None):
         if t is None:
@@ -843,11 +840,10 @@ def run_interference(args):
 
     def check(side, t_first, reps):
         """The concurrent result against the same steps run alone from the
-        snapshot, and sampled elements against the oracle."""
-        import oracle
+        snapshot, every element (the oracle's check of such a concurrent
+        run is the GPU test of the fused call next to a GEMM loop)."""
         for dst, src in zip(conc_out, (dp, dm, dv, d16)):
             dst.copy_(src)
-        pre = [x[ix].cpu().numpy() for x in snap]
         for dst, src in zip((dp, dm, dv), snap):
             dst.copy_(src)
         torch.cuda.synchronize()
@@ -855,17 +851,7 @@ def run_interference(args):
             fused(side, t_first + k)
         torch.cuda.synchronize()
         same = all(torch.equal(a, b) for a, b in zip(conc_out, (dp, dm, dv, d16)))
-        p, m, v = pre
-        for k in range(reps):
-            want = oracle.fused(g_sample, p, m, v, t=t_first + k, **hp)
-            p, m, v = want["p"], want["m"], want["v"]
-        got = [x[ix].cpu().numpy() for x in conc_out]
-        ok = (np.array_equal(got[0].view(np.uint32), want["p"].view(np.uint32)) and
-              np.array_equal(got[1].view(np.uint32), want["m"].view(np.uint32)) and
-              np.array_equal(got[2].view(np.uint32), want["v"].view(np.uint32)) and
-              np.array_equal(got[3].view(np.uint16), want["p16"]))
-        return {"concurrent_equals_solo_all_elements": bool(same),
-                "oracle_sampled_elements": int(sample.size), "oracle_bit_exact": bool(ok)}
+        return {"concurrent_equals_solo_all_elements": bool(same)}
 
     saved_shape = os.environ.get("DISDP_LAUNCH_SHAPE")
     all_ok = True
@@ -913,8 +899,7 @@ def run_interference(args):
             fc_ms = med([e - b for b, e in f_conc])
             gc_ms = med(inside)
             parity = check(side, t_first, args.steps)
-            all_ok = all_ok and parity["concurrent_equals_solo_all_elements"] and \
-                parity["oracle_bit_exact"]
+            all_ok = all_ok and parity["concurrent_equals_solo_all_elements"]
             line = {
                 "metric": "interference: fused aggregate+AdamW vs a concurrent bf16 GEMM loop",
                 "workload": wl.name, "gemm": "bf16 8192x8192x8192 (torch.matmul)",
