@@ -855,80 +855,82 @@ def run_interference(args):
 
     saved_shape = os.environ.get("DISDP_LAUNCH_SHAPE")
     all_ok = True
-    for shape in args.shape.split(","):
-        os.environ["DISDP_LAUNCH_SHAPE"] = shape
-        for k in [int(x) for x in args.cu_split.split(",")]:
-            if k == 0:
-                # both streams on every CU: a CU-masked stream has a hardware
-                # queue of its own, whereas two ordinary streams can share
-                # one and then run one after the other
-                side, h1, hip = _cu_mask_stream(0, n_cu, n_cu)
-                comp, h2, _ = _cu_mask_stream(0, n_cu, n_cu)
-            else:
-                side, h1, hip = _cu_mask_stream(0, k, n_cu)
-                comp, h2, _ = _cu_mask_stream(k, n_cu - k, n_cu)
-            handles = [(hip, h1), (hip, h2)]
-            for _ in range(2):
-                fused(side)
-                gemm(comp)
-            torch.cuda.synchronize()
-            origin = torch.cuda.Event(enable_timing=True)
-            origin.record(torch.cuda.current_stream())
-            torch.cuda.synchronize()
-            ev = enqueue(side, fused, args.steps)
-            torch.cuda.synchronize()
-            f_solo = spans(origin, ev)
-            n_gemm_solo = 30
-            ev = enqueue(comp, gemm, n_gemm_solo)
-            torch.cuda.synchronize()
-            g_solo = spans(origin, ev)
-            fs_ms = med([e - b for b, e in f_solo])
-            gs_ms = med([e - b for b, e in g_solo])
-            n_gemm = int(3 * args.steps * fs_ms / gs_ms) + 10
-            for dst, src in zip(snap, (dp, dm, dv)):
-                dst.copy_(src)
-            torch.cuda.synchronize()
-            t_first = t_state[0] + 1
-            evg = enqueue(comp, gemm, n_gemm)
-            evf = enqueue(side, fused, args.steps)
-            torch.cuda.synchronize()
-            g_conc, f_conc = spans(origin, evg), spans(origin, evf)
-            w0, w1 = min(b for b, _ in f_conc), max(e for _, e in f_conc)
-            inside = [e - b for b, e in g_conc if b >= w0 and e <= w1]
-            busy = sum(max(0.0, min(e, w1) - max(b, w0)) for b, e in g_conc) / (w1 - w0)
-            fc_ms = med([e - b for b, e in f_conc])
-            gc_ms = med(inside)
-            parity = check(side, t_first, args.steps)
-            all_ok = all_ok and parity["concurrent_equals_solo_all_elements"]
-            line = {
-                "metric": "interference: fused aggregate+AdamW vs a concurrent bf16 GEMM loop",
-                "workload": wl.name, "gemm": "bf16 8192x8192x8192 (torch.matmul)",
-                "launch_shape": shape,
-                "cu_split": None if k == 0 else {"fused_cus": k, "gemm_cus": n_cu - k},
-                "fused_solo_ms": round(fs_ms, 4), "fused_concurrent_ms": round(fc_ms, 4),
-                "fused_slowdown": round(fc_ms / fs_ms, 3),
-                "fused_solo_TBps": round(wl.n * 58 / (fs_ms * 1e-3) / 1e12, 3),
-                "gemm_solo_ms": round(gs_ms, 4),
-                "gemm_concurrent_ms": None if gc_ms is None else round(gc_ms, 4),
-                "gemm_slowdown": None if gc_ms is None else round(gc_ms / gs_ms, 3),
-                "gemm_solo_tflops": round(2 * 8192**3 / (gs_ms * 1e-3) / 1e12, 1),
-                "gemms_inside_fused_window": len(inside),
-                "gemm_busy_frac": round(busy, 3),
-                "fused_reps": args.steps,
-                "phases": {"warmup_fused_and_gemm": 2, "fused_solo": args.steps,
-                           "gemm_solo": n_gemm_solo, "gemm_concurrent": n_gemm,
-                           "fused_concurrent": args.steps, "fused_check": args.steps},
-                "parity": parity,
-                "streams": "default priority, CU-masked" + (" (full mask: every CU)" if k == 0 else ""),
-            }
-            print(json.dumps(line), flush=True)
-            torch.cuda.synchronize()
-            for hip, h in handles:
-                hip.hipStreamDestroy(h)
-    if saved_shape is None:
-        os.environ.pop("DISDP_LAUNCH_SHAPE", None)
-    else:
-        os.environ["DISDP_LAUNCH_SHAPE"] = saved_shape
+    try:
+        for shape in args.shape.split(","):
+            os.environ["DISDP_LAUNCH_SHAPE"] = shape
+            for k in [int(x) for x in args.cu_split.split(",")]:
+                if k == 0:
+                    # both streams on every CU: a CU-masked stream has a hardware
+                    # queue of its own, whereas two ordinary streams can share
+                    # one and then run one after the other
+                    side, h1, hip = _cu_mask_stream(0, n_cu, n_cu)
+                    comp, h2, _ = _cu_mask_stream(0, n_cu, n_cu)
+                else:
+                    side, h1, hip = _cu_mask_stream(0, k, n_cu)
+                    comp, h2, _ = _cu_mask_stream(k, n_cu - k, n_cu)
+                handles = [(hip, h1), (hip, h2)]
+                for _ in range(2):
+                    fused(side)
+                    gemm(comp)
+                torch.cuda.synchronize()
+                origin = torch.cuda.Event(enable_timing=True)
+                origin.record(torch.cuda.current_stream())
+                torch.cuda.synchronize()
+                ev = enqueue(side, fused, args.steps)
+                torch.cuda.synchronize()
+                f_solo = spans(origin, ev)
+                n_gemm_solo = 30
+                ev = enqueue(comp, gemm, n_gemm_solo)
+                torch.cuda.synchronize()
+                g_solo = spans(origin, ev)
+                fs_ms = med([e - b for b, e in f_solo])
+                gs_ms = med([e - b for b, e in g_solo])
+                n_gemm = int(3 * args.steps * fs_ms / gs_ms) + 10
+                for dst, src in zip(snap, (dp, dm, dv)):
+                    dst.copy_(src)
+                torch.cuda.synchronize()
+                t_first = t_state[0] + 1
+                evg = enqueue(comp, gemm, n_gemm)
+                evf = enqueue(side, fused, args.steps)
+                torch.cuda.synchronize()
+                g_conc, f_conc = spans(origin, evg), spans(origin, evf)
+                w0, w1 = min(b for b, _ in f_conc), max(e for _, e in f_conc)
+                inside = [e - b for b, e in g_conc if b >= w0 and e <= w1]
+                busy = sum(max(0.0, min(e, w1) - max(b, w0)) for b, e in g_conc) / (w1 - w0)
+                fc_ms = med([e - b for b, e in f_conc])
+                gc_ms = med(inside)
+                parity = check(side, t_first, args.steps)
+                all_ok = all_ok and parity["concurrent_equals_solo_all_elements"]
+                line = {
+                    "metric": "interference: fused aggregate+AdamW vs a concurrent bf16 GEMM loop",
+                    "workload": wl.name, "gemm": "bf16 8192x8192x8192 (torch.matmul)",
+                    "launch_shape": shape,
+                    "cu_split": None if k == 0 else {"fused_cus": k, "gemm_cus": n_cu - k},
+                    "fused_solo_ms": round(fs_ms, 4), "fused_concurrent_ms": round(fc_ms, 4),
+                    "fused_slowdown": round(fc_ms / fs_ms, 3),
+                    "fused_solo_TBps": round(wl.n * 58 / (fs_ms * 1e-3) / 1e12, 3),
+                    "gemm_solo_ms": round(gs_ms, 4),
+                    "gemm_concurrent_ms": None if gc_ms is None else round(gc_ms, 4),
+                    "gemm_slowdown": None if gc_ms is None else round(gc_ms / gs_ms, 3),
+                    "gemm_solo_tflops": round(2 * 8192**3 / (gs_ms * 1e-3) / 1e12, 1),
+                    "gemms_inside_fused_window": len(inside),
+                    "gemm_busy_frac": round(busy, 3),
+                    "fused_reps": args.steps,
+                    "phases": {"warmup_fused_and_gemm": 2, "fused_solo": args.steps,
+                               "gemm_solo": n_gemm_solo, "gemm_concurrent": n_gemm,
+                               "fused_concurrent": args.steps, "fused_check": args.steps},
+                    "parity": parity,
+                    "streams": "default priority, CU-masked" + (" (full mask: every CU)" if k == 0 else ""),
+                }
+                print(json.dumps(line), flush=True)
+                torch.cuda.synchronize()
+                for hip, h in handles:
+                    hip.hipStreamDestroy(h)
+    finally:
+        if saved_shape is None:
+            os.environ.pop("DISDP_LAUNCH_SHAPE", None)
+        else:
+            os.environ["DISDP_LAUNCH_SHAPE"] = saved_shape
     if not all_ok:
         raise SystemExit("interference: a concurrent result differs from the solo run")
 

@@ -133,6 +133,24 @@ def run_fused_case(W, gdtype, mode, n, t=3, frac_bits=24, offsets=(0, 0),
     return got, want
 
 
+def cu_masked_stream(n_cus):
+    """A default-priority stream restricted to the first n_cus CUs
+    (hipExtStreamCreateWithCUMask on torch's HIP runtime): (torch stream,
+    raw handle, runtime library).  A CU-masked stream has a hardware queue
+    of its own.  The caller destroys the handle with hipStreamDestroy."""
+    import ctypes
+    t_ = torch()
+    total = t_.cuda.get_device_properties(0).multi_processor_count
+    hip = ctypes.CDLL("libamdhip64.so.7")          # torch's runtime, already loaded
+    words = (total + 31) // 32
+    mask = (ctypes.c_uint32 * words)()
+    for cu in range(min(n_cus, total)):
+        mask[cu // 32] |= 1 << (cu % 32)
+    h = ctypes.c_void_p()
+    assert hip.hipExtStreamCreateWithCUMask(ctypes.byref(h), ctypes.c_uint32(words), mask) == 0
+    return t_.cuda.ExternalStream(h.value), h, hip
+
+
 def host_threads() -> int:
     """Host threads a test may use (the CPU share of one GPU: at most 16)."""
     import os

@@ -13,7 +13,7 @@ import pytest
 
 import oracle
 import synth
-from gpu_common import (HP, assert_parity, bits, f32_same, run_fused_case,
+from gpu_common import (HP, assert_parity, bits, cu_masked_stream, f32_same, run_fused_case,
                         to_dev, to_host, torch)
 
 pytestmark = pytest.mark.gpu
@@ -617,21 +617,6 @@ def test_one_hip_graph_serves_every_optimizer_step(mode):
     del graph
 
 
-def _cu_masked_stream(n_cus):
-    """A default-priority stream restricted to the first n_cus CUs
-    (hipExtStreamCreateWithCUMask on torch's HIP runtime)."""
-    import ctypes
-    t_ = torch()
-    total = t_.cuda.get_device_properties(0).multi_processor_count
-    hip = ctypes.CDLL("libamdhip64.so.7")          # torch's runtime, already loaded
-    words = (total + 31) // 32
-    mask = (ctypes.c_uint32 * words)()
-    for cu in range(min(n_cus, total)):
-        mask[cu // 32] |= 1 << (cu % 32)
-    h = ctypes.c_void_p()
-    assert hip.hipExtStreamCreateWithCUMask(ctypes.byref(h), ctypes.c_uint32(words), mask) == 0
-    return t_.cuda.ExternalStream(h.value), h, hip
-
 
 @pytest.mark.parametrize("mode", ["fp32", "fixed"])
 def test_fused_on_cu_masked_streams(mode):
@@ -654,7 +639,7 @@ def test_fused_on_cu_masked_streams(mode):
     assert_parity({"p": to_host(base[0]), "m": to_host(base[1]), "v": to_host(base[2]),
                    "p16": to_host(base[3])}, want, f"default stream {mode}")
     for n_cus in (32, 200):
-        s, h, hip = _cu_masked_stream(n_cus)
+        s, h, hip = cu_masked_stream(n_cus)
         try:
             st = [to_dev(x) for x in (p, m, v)] + [to_dev(np.zeros(n, np.uint16))]
             t_.cuda.synchronize()
@@ -1270,7 +1255,7 @@ def test_multi_tensor_call_with_pinned_host_state_and_on_a_cu_masked_stream():
             for dst, src in zip((dp, dm, dv, d16), st):
                 dst.copy_(src)
         t_.cuda.synchronize()
-        s, h, hip = _cu_masked_stream(n_cus)
+        s, h, hip = cu_masked_stream(n_cus)
         try:
             dd.aggregate_adam_multi(a, stream=s, **kw)
             s.synchronize()

@@ -12,23 +12,9 @@ import pytest
 
 import oracle
 import synth
-from gpu_common import HP, assert_parity, run_fused_case, to_dev, to_host, torch
+from gpu_common import (HP, assert_parity, cu_masked_stream, run_fused_case, to_dev, to_host,
+                        torch)
 
-
-def _cu_masked_stream(n_cus):
-    """A default-priority stream on the first n_cus CUs
-    (hipExtStreamCreateWithCUMask on torch's HIP runtime)."""
-    import ctypes
-    t_ = torch()
-    total = t_.cuda.get_device_properties(0).multi_processor_count
-    hip = ctypes.CDLL("libamdhip64.so.7")          # torch's runtime, already loaded
-    words = (total + 31) // 32
-    mask = (ctypes.c_uint32 * words)()
-    for cu in range(min(n_cus, total)):
-        mask[cu // 32] |= 1 << (cu % 32)
-    h = ctypes.c_void_p()
-    assert hip.hipExtStreamCreateWithCUMask(ctypes.byref(h), ctypes.c_uint32(words), mask) == 0
-    return t_.cuda.ExternalStream(h.value), h, hip
 
 pytestmark = pytest.mark.gpu
 
@@ -132,7 +118,7 @@ def test_fused_next_to_a_gemm_loop_equals_solo(shape, mode):
     # streams with a full CU mask: each has a hardware queue of its own, so
     # the GEMMs and the fused steps really run at the same time
     total = t_.cuda.get_device_properties(0).multi_processor_count
-    (side, hs, hip), (comp, hc, _) = _cu_masked_stream(total), _cu_masked_stream(total)
+    (side, hs, hip), (comp, hc, _) = cu_masked_stream(total), cu_masked_stream(total)
 
     def run(concurrent):
         st = [x.clone() for x in (p0, m0, v0)] + [t_.empty(n, dtype=t_.int16, device="cuda")]
