@@ -430,3 +430,43 @@ def test_full_size_int32_contributions_equal_the_float_path():
     finally:
         del gf, gi, a, b, a16, b16, ai, bi, sh
         t_.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("W,gdtype,mode,n", [(64, "bf16", "fp32", (1 << 28) + 3),
+                                             (33, "f32", "fixed", (1 << 27) + 5)])
+def test_run_time_worker_counts_at_scale(W, gdtype, mode, n):
+    """The run-time worker-count kernels (W outside the compile-time set)
+    at scale: every element of t = 1 against the oracle, the int32
+    aggregate included in fixed mode."""
+    import paper_2409_00918_amd as dd
+    t_ = torch()
+    gb = 2 if gdtype == "bf16" else 4
+    fixed = mode == "fixed"
+    need = n * (W * gb + 12 + 2 + (4 if fixed else 0) + 12)
+    free, _ = t_.cuda.mem_get_info()
+    if need > 0.9 * free:
+        pytest.skip("not enough device memory")
+    print(f"[fullsize] run-time W={W} {gdtype} {mode} n={n}", flush=True)
+    dg = synth.device_grads(77, 1, W, n, 1e-4, gdtype=gdtype, outlier_frac=0.01,
+                            outlier_scale=100.0)
+    dp, dm, dv = synth.device_state(77, n, 0.02)
+    d16 = t_.empty(n, dtype=t_.int16, device="cuda")
+    dai = t_.empty(n, dtype=t_.int32, device="cuda") if fixed else None
+    snap = [x.clone() for x in (dp, dm, dv)]
+    hp = dict(lr=np.float32(1e-4), beta1=np.float32(0.9), beta2=np.float32(0.95),
+              eps=np.float32(1e-8), wd=np.float32(0.1))
+    try:
+        dd.aggregate_adam(dg, dp, dm, dv, d16, lr=hp["lr"], beta1=hp["beta1"],
+                          beta2=hp["beta2"], eps=hp["eps"], weight_decay=hp["wd"], step=1,
+                          mode=mode, frac_bits=24, agg_out_i32=dai)
+        t_.cuda.synchronize()
+        post = {"p": dp, "m": dm, "v": dv, "p16": d16}
+        if fixed:
+            post["agg_i32"] = dai
+        bad = whole_shard_mismatches(dg, snap, post, gdtype=gdtype, mode=mode, frac_bits=24,
+                                     t=1, hp=hp, label=f"run-time W={W} {gdtype} {mode}")
+        assert bad["elements"] == n
+        assert all(c == 0 for k, c in bad.items() if k != "elements"), bad
+    finally:
+        del dg, dp, dm, dv, d16, dai, snap
+        t_.cuda.empty_cache()

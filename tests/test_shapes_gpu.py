@@ -167,3 +167,13 @@ def test_fused_next_to_a_gemm_loop_equals_solo(shape, mode):
     assert_parity({"p": to_host(conc[0][ix]), "m": to_host(conc[1][ix]),
                    "v": to_host(conc[2][ix]), "p16": to_host(conc[3][ix])}, want,
                   f"{shape} {mode} concurrent vs oracle")
+
+
+@pytest.mark.parametrize("value", ["SHARED", "bogus", ""])
+def test_unrecognised_launch_shape_means_the_default(value, monkeypatch):
+    """Only the exact value "shared" selects the shared shape; anything else
+    launches the default shape, with the same (oracle-checked) bits."""
+    monkeypatch.setenv("DISDP_LAUNCH_SHAPE", value)
+    for W, gdtype, mode in ((8, "f32", "fp32"), (24, "f32", "fixed")):
+        got, want = run_fused_case(W, gdtype, mode, 100_003, t=2, seed=400 + W)
+        assert_parity(got, want, f"DISDP_LAUNCH_SHAPE={value!r} W={W} {mode}")
