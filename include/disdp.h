@@ -82,7 +82,13 @@
  *             Outputs must not overlap one another nor any input; p, m and
  *             v are updated in place (each is its own input).  Contributions
  *             may overlap each other (the same buffer may be passed twice).
- *             A launch failure returns DISDP_ERR_HIP.
+ *             A launch failure returns DISDP_ERR_HIP.  A runtime query
+ *             the library makes (pointer attributes, the stream's CU mask)
+ *             that fails leaves no error behind when none was pending
+ *             before the call; when the caller already had one pending, the
+ *             error state is left set (the runtime keeps a single last
+ *             error, which the failed query may have replaced), so
+ *             hipGetLastError still reports an error.
  * Numerics    IEEE binary32, round to nearest even, one rounding per
  *             operation, no fused multiply-add, denormals kept; results are
  *             a deterministic function of the inputs (no atomics, no
