@@ -617,6 +617,23 @@ void error_case()
            DISDP_OK, label);
     HIP_OK(hipDeviceSynchronize());
     HIP_OK(hipGetLastError());  // the refused pointer query left no sticky error
+    // An error the caller has not read yet survives a call whose pointer
+    // query fails: make one on the host (an out-of-range device index; no
+    // device work), let the library refuse pageable memory, and the error
+    // is still reported, then cleared by reading it.
+    int count = 0;
+    HIP_OK(hipGetDeviceCount(&count));
+    if (hipSetDevice(count + 7) == hipSuccess) {
+        std::printf("FAIL %s: device %d accepted\n", label, count + 7);
+        ++failures;
+    }
+    expect(disdp_aggregate(gp, 1, DISDP_DT_F32, n, DISDP_AGG_FP32, 0, b, nullptr, 0),
+           DISDP_ERR_INVALID_ARG, label);
+    if (hipGetLastError() == hipSuccess) {
+        std::printf("FAIL %s: a pending error was cleared by the library\n", label);
+        ++failures;
+    }
+    HIP_OK(hipGetLastError());  // read once: gone
     std::printf("%s %s\n", failures ? "FAIL" : "ok", label);
     HIP_OK(hipFree(a));
     HIP_OK(hipFree(b));
